@@ -1,0 +1,24 @@
+"""The paper's printed search space (Appendix C.5) maps onto the op schema."""
+import json
+import os
+
+from synth import config as C
+
+HERE = os.path.dirname(__file__)
+
+
+def test_search_space_table_maps_to_ops():
+    t = json.load(open(os.path.join(HERE, "golden", "search_space.json")))
+    assert len(t["grid"]) == 12 and len(t["ashape"]) == 3 and len(t["vslash"]) == 9
+    for mode, h, v, s, mx in t["grid"]:
+        assert mx == C.MAX_STRIDE
+        op = C.grid_frame(256, h, v, s) if mode == "frame_stride" else C.grid_window(256, 8, h, v, s)
+        assert op.kind == C.OP_GRID and (op.use_h, op.use_v, op.use_s) == (h, v, s)
+        assert 1 <= op.stride_lo <= op.stride_hi <= mx
+    for sink, local in t["ashape"]:
+        op = C.ashape(sink, local)
+        assert (op.sink, op.local) == (sink, local)
+    for nv, ns in t["vslash"]:
+        op = C.vslash(nv, ns)
+        assert (op.n_vertical, op.n_slash) == (nv, ns)
+    assert t["last_q"]["value"] == C.LAST_Q

@@ -1,0 +1,208 @@
+"""Pins of the oracle's block sets: closed forms == literal lift, reductions.
+
+The literal lift enumerates every (query, key) token pair (causal by original
+positions, plus each row's own key block); the closed forms compute the same
+set per op without enumeration. They are independent code paths in
+oracle/plan.py and must agree exactly.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+from oracle import plan as P
+from synth import config as C
+
+FLAGS = list(itertools.product([False, True], repeat=3))   # (h, v, s)
+
+
+def _same(hp):
+    lifted = P.lift_blocks(hp)
+    assert len(lifted) == len(hp.blocks)
+    for i, (a, b) in enumerate(zip(hp.blocks, lifted)):
+        assert np.array_equal(a, b), (i, a, b)
+
+
+def _grid_plan(L, s, p, h, v, sflag):
+    st = P.grid_state(C.grid(s, s, h, v, sflag), L, s, p)
+    return P.assemble(C.HEAD_GLOBAL, L, None, {"g": st})
+
+
+@pytest.mark.parametrize("L", [333, 128])
+def test_grid_closed_form_exhaustive_small_strides(L):
+    for s in range(1, 33):
+        for p in range(s):
+            for h, v, sf in FLAGS:
+                _same(_grid_plan(L, s, p, h, v, sf))
+
+
+def test_grid_closed_form_frame_sized_strides():
+    rng = np.random.default_rng(0)
+    for L in (2000, 4096, 1111):
+        for s in (63, 64, 65, 100, 127, 196, 252, 255, 256, 500):
+            for h, v, sf in FLAGS:
+                p = int(rng.integers(0, s))
+                _same(_grid_plan(L, s, p, h, v, sf))
+
+
+def test_grid_reductions():
+    L = 700
+    hp = _grid_plan(L, 1, 0, False, False, True)          # one group, same phase = dense
+    nb = hp.nbq
+    assert all(np.array_equal(hp.blocks[i], np.arange(i + 1)) for i in range(nb))
+    assert np.array_equal(hp.qperm[:L], np.arange(L))
+    hp = _grid_plan(L, 9, 4, False, False, False)         # no lines: own blocks only
+    assert all(np.array_equal(hp.blocks[i], [i]) for i in range(nb))
+
+
+def _id_plan(L, st):
+    return P.assemble(C.HEAD_GLOBAL, L, None, {"g": st})
+
+
+def test_ashape_closed_form_and_reductions():
+    rng = np.random.default_rng(1)
+    for L in (300, 1000, 64 * 9):
+        for sink, local in [(128, 256), (7, 64), (0, 100), (128, 0), (1, 1), (500, 50)]:
+            _same(_id_plan(L, P.OpState(C.OP_ASHAPE, C.ashape(sink, local), L=L)))
+        dense = [np.arange(i + 1) for i in range((L + 63) // 64)]
+        for sink, local in [(L, 1), (0, L), (L + 5, L + 5)]:
+            hp = _id_plan(L, P.OpState(C.OP_ASHAPE, C.ashape(sink, local), L=L))
+            assert all(np.array_equal(a, b) for a, b in zip(hp.blocks, dense))
+
+
+def test_vslash_closed_form_and_reductions():
+    rng = np.random.default_rng(2)
+    for L in (300, 1000, 64 * 7 + 1):
+        for nv, ns in [(10, 10), (1, 50), (0, 3), (40, 0), (200, 200)]:
+            vs = np.sort(rng.choice(L, size=min(nv, L), replace=False))
+            ss = np.sort(rng.choice(L, size=min(ns, L), replace=False))
+            st = P.OpState(C.OP_VSLASH, C.vslash(nv, ns), vsel=vs, ssel=ss, L=L)
+            _same(_id_plan(L, st))
+        dense = [np.arange(i + 1) for i in range((L + 63) // 64)]
+        for vs, ss in [(np.arange(L), np.zeros(0, np.int64)), (np.zeros(0, np.int64), np.arange(L))]:
+            hp = _id_plan(L, P.OpState(C.OP_VSLASH, C.vslash(0, 0), vsel=vs, ssel=ss, L=L))
+            assert all(np.array_equal(a, b) for a, b in zip(hp.blocks, dense))
+
+
+def _random_layout(rng, S, nmod=2, minseg=1, maxseg=300):
+    segs, m, n = [], 0, 0
+    while n < S:
+        ln = int(min(S - n, rng.integers(minseg, maxseg + 1)))
+        segs.append(np.full(ln, m, np.uint8))
+        n += ln
+        m = (m + int(rng.integers(1, nmod))) % nmod
+    return np.concatenate(segs)
+
+
+def _rand_identity_op(rng, L, allow=("dense", "ashape", "vslash")):
+    k = allow[int(rng.integers(0, len(allow)))]
+    if k == "dense":
+        return P.OpState(C.OP_DENSE, C.dense(), L=L)
+    if k == "ashape":
+        sink, local = int(rng.integers(0, 200)), int(rng.integers(0, 300))
+        return P.OpState(C.OP_ASHAPE, C.ashape(sink, local), L=L)
+    nv, ns = int(rng.integers(0, 40)), int(rng.integers(0, 40))
+    vs = np.sort(rng.choice(L, size=min(nv, L), replace=False))
+    ss = np.sort(rng.choice(L, size=min(ns, L), replace=False))
+    return P.OpState(C.OP_VSLASH, C.vslash(nv, ns), vsel=vs, ssel=ss, L=L)
+
+
+def test_qboundary_closed_form_random_layouts():
+    rng = np.random.default_rng(3)
+    for trial in range(25):
+        S = int(rng.integers(100, 1500))
+        mod = _random_layout(rng, S, nmod=int(rng.integers(2, 4)), maxseg=int(rng.integers(5, 400)))
+        ops = {("q", int(m)): _rand_identity_op(rng, S) for m in np.unique(mod)}
+        hp = P.assemble(C.HEAD_QBOUNDARY, S, mod, ops)
+        _same(hp)
+
+
+def test_2d_closed_form_random_layouts():
+    rng = np.random.default_rng(4)
+    for trial in range(25):
+        S = int(rng.integers(100, 1500))
+        mod = _random_layout(rng, S, nmod=int(rng.integers(2, 4)), maxseg=int(rng.integers(5, 400)))
+        mods = [int(m) for m in np.unique(mod)]
+        T = {m: np.nonzero(mod == m)[0] for m in mods}
+        ops = {}
+        for m in mods:
+            L = len(T[m])
+            if rng.random() < 0.4 and L >= 2:
+                s = int(rng.integers(1, max(2, L // 2) + 1))
+                f = FLAGS[int(rng.integers(0, 8))]
+                ops[("i", m)] = P.grid_state(C.grid(s, s, *f), L, s, int(rng.integers(0, s)))
+            else:
+                ops[("i", m)] = _rand_identity_op(rng, L)
+        for mq in mods:
+            for mk in mods:
+                if mq == mk:
+                    continue
+                r = rng.random()
+                L = len(T[mk])
+                if r < 0.3:
+                    ops[("x", mq, mk)] = P.OpState(C.OP_NONE, C.none(), L=L)
+                elif r < 0.6:
+                    ops[("x", mq, mk)] = P.OpState(C.OP_DENSE, C.dense(), L=L)
+                else:
+                    n = int(rng.integers(0, 30))
+                    sel = np.sort(rng.choice(L, size=min(n, L), replace=False))
+                    ops[("x", mq, mk)] = P.OpState(C.OP_VERT, C.vert(n), vsel=sel, L=L)
+        hp = P.assemble(C.HEAD_2D, S, mod, ops)
+        _same(hp)
+
+
+def test_boundary_heads_reduce_to_global_on_one_modality():
+    rng = np.random.default_rng(5)
+    S = 777
+    for trial in range(6):
+        st = _rand_identity_op(rng, S)
+        g = P.assemble(C.HEAD_GLOBAL, S, None, {"g": st})
+        q = P.assemble(C.HEAD_QBOUNDARY, S, None, {("q", 0): st})
+        d = P.assemble(C.HEAD_2D, S, None, {("i", 0): st})
+        for hp in (q, d):
+            assert np.array_equal(hp.qperm, g.qperm)
+            assert all(np.array_equal(a, b) for a, b in zip(hp.blocks, g.blocks))
+    st = P.grid_state(C.grid(13, 13), S, 13, 5)
+    g = P.assemble(C.HEAD_GLOBAL, S, None, {"g": st})
+    d = P.assemble(C.HEAD_2D, S, None, {("i", 0): st})
+    assert np.array_equal(d.qperm, g.qperm) and np.array_equal(d.kperm, g.kperm)
+    assert all(np.array_equal(a, b) for a, b in zip(d.blocks, g.blocks))
+
+
+def test_2d_all_dense_pairs_is_dense_attention_mask():
+    rng = np.random.default_rng(6)
+    S = 900
+    mod = _random_layout(rng, S, nmod=3, maxseg=200)
+    mods = [int(m) for m in np.unique(mod)]
+    T = {m: np.nonzero(mod == m)[0] for m in mods}
+    ops = {("i", m): P.OpState(C.OP_DENSE, C.dense(), L=len(T[m])) for m in mods}
+    ops.update({("x", a, b): P.OpState(C.OP_DENSE, C.dense(), L=len(T[b]))
+                for a in mods for b in mods if a != b})
+    hp = P.assemble(C.HEAD_2D, S, mod, ops)
+    for q in rng.choice(S, 50, replace=False):
+        assert np.array_equal(P.element_mask_row(hp, int(q)), np.arange(q + 1))
+
+
+def test_permutations_are_bijections():
+    rng = np.random.default_rng(7)
+    S = 1000
+    mod = _random_layout(rng, S, nmod=2, maxseg=150)
+    T = {m: np.nonzero(mod == m)[0] for m in (0, 1)}
+    ops = {("i", 0): P.OpState(C.OP_DENSE, C.dense(), L=len(T[0])),
+           ("i", 1): P.grid_state(C.grid(7, 7), len(T[1]), 7, 2),
+           ("x", 0, 1): P.OpState(C.OP_DENSE, C.dense(), L=len(T[1])),
+           ("x", 1, 0): P.OpState(C.OP_NONE, C.none(), L=len(T[0]))}
+    for kind, o in [(C.HEAD_2D, ops),
+                    (C.HEAD_QBOUNDARY, {("q", 0): ops[("i", 0)], ("q", 1): ops[("i", 0)]})]:
+        hp = P.assemble(kind, S, mod, o)
+        for perm in (hp.qperm, hp.kperm):
+            assert len(perm) % 64 == 0
+            live = perm[perm >= 0]
+            assert sorted(live.tolist()) == list(range(S))
+            # unpermute(permute(x)) == x
+            x = np.random.default_rng(0).random(S)
+            y = np.zeros(len(perm))
+            y[perm >= 0] = x[live]
+            back = np.zeros(S)
+            back[live] = y[perm >= 0]
+            assert np.array_equal(back, x)
