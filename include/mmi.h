@@ -1,0 +1,196 @@
+/*
+ * mmi.h - C-ABI of the MI355X modality-aware permutation sparse attention
+ * library (libmmi.so): the pre-filling hot path of MMInference
+ * (arXiv 2504.16083).
+ *
+ * Problem statement (Section 3, Algorithms 1-3): inputs are Q, K, V of one
+ * attention layer, the modality type index i_m of every token and the
+ * per-head pattern chosen offline (Algorithm 4 outputs it; here it is an
+ * input); the output is the attention output y (and optionally each row's
+ * log-sum-exp). For each head the library estimates the pattern parameters
+ * online from the last queries, builds the Q/K/V permutation and the block
+ * index, runs a block-sparse causal FlashAttention-style kernel over the
+ * selected 64x64 blocks and writes the output back in original token order.
+ *
+ * Conventions shared by every entry point:
+ *   - All functions return an int status (MMI_OK or a negative MMI_ERR_*).
+ *     On error nothing is written to caller buffers; mmi_last_error() gives
+ *     a thread-local message. No C++ exception crosses this boundary.
+ *   - Tensor pointers are DEVICE pointers owned by the caller; the library
+ *     never frees them nor keeps them past the call that receives them.
+ *     Work is enqueued asynchronously on the caller's HIP stream
+ *     (hipStream_t passed as void*, NULL = the default stream); every
+ *     argument is validated on the host before the first launch.
+ *   - Shapes: one layer, batch 1, head_dim D = 128, block size 64, causal,
+ *     bfloat16 Q/K/V/O. Hq query heads share Hkv KV heads (GQA): query head
+ *     h reads KV head h / (Hq / Hkv). Element strides are given per token
+ *     and per head; the head dimension must be contiguous and every row
+ *     16-byte aligned. Stride 0 means the packed [S, H, 128] layout.
+ *   - The output O must not alias Q, K or V. A plan is not thread-safe.
+ */
+#ifndef MMI_H
+#define MMI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MMI_ABI_VERSION 1
+#define MMI_MAX_MODALITIES 8
+#define MMI_HEAD_DIM 128
+#define MMI_BLOCK 64
+#define MMI_LAST_Q 64          /* estimation rows, Section 4.1 (last_q = 64) */
+#define MMI_MAX_STRIDE 1024    /* Grid max stride, Appendix C.5 table */
+#define MMI_MAX_SEQ (1 << 21)  /* largest supported S (2,097,152 tokens) */
+
+/* status codes */
+#define MMI_OK 0
+#define MMI_ERR_INVALID_ARG -1  /* NULL pointer, negative size, bad stride  */
+#define MMI_ERR_UNSUPPORTED -2  /* D != 128, block != 64, Hq % Hkv != 0, S too large */
+#define MMI_ERR_BAD_CONFIG -3   /* an op/head kind or parameter out of range */
+#define MMI_ERR_OOM -4          /* device allocation failed */
+#define MMI_ERR_HIP -5          /* a HIP runtime call failed (text in mmi_last_error) */
+#define MMI_ERR_STATE -6        /* call out of order (e.g. export before create) */
+#define MMI_ERR_INTERNAL -7
+
+/* Op kinds. One op describes a token predicate pred(q, k) in one coordinate
+ * system; the selected blocks are the causal block lift of it (see
+ * mmi_plan_create). */
+#define MMI_OP_NONE 0    /* no key selected (2D-Boundary cross pairs only) */
+#define MMI_OP_DENSE 1   /* every causal key */
+#define MMI_OP_ASHAPE 2  /* k < sink or q - k < local (Appendix C.3)                */
+#define MMI_OP_VSLASH 3  /* k in top-n_vertical columns or q - k in top-n_slash      */
+                         /* diagonals of the estimate (Appendix C.3)                */
+#define MMI_OP_GRID 4    /* Grid head (Algorithm 1): stride/phase searched over      */
+                         /* [stride_lo, stride_hi]; q = k (mod s) if use_s, k = p   */
+                         /* (mod s) if use_v, q = p (mod s) if use_h                */
+#define MMI_OP_VERT 5    /* k in the top-n_vertical key columns of the key modality, */
+                         /* estimated from the query modality's final queries        */
+                         /* (2D-Boundary cross pairs only)                            */
+
+/* Head kinds. */
+#define MMI_HEAD_GLOBAL 0     /* one op over all rows: No-Boundary / K-Boundary (Sec. 3.2) */
+#define MMI_HEAD_QBOUNDARY 1  /* Algorithm 2: queries grouped by modality, op per modality */
+#define MMI_HEAD_2D 2         /* Algorithm 3: Q and K grouped by modality, op per pair    */
+
+typedef struct mmi_op {
+  int32_t kind;                  /* MMI_OP_* */
+  int32_t sink, local;           /* ASHAPE: sink >= 0, local >= 0 */
+  int32_t n_vertical, n_slash;   /* VSLASH (both), VERT (n_vertical); >= 0 */
+  int32_t stride_lo, stride_hi;  /* GRID: 1 <= lo <= hi <= MMI_MAX_STRIDE */
+  int32_t use_h, use_v, use_s;   /* GRID line flags (0/1) */
+} mmi_op;
+
+typedef struct mmi_head_cfg {
+  int32_t kind;                  /* MMI_HEAD_* */
+  mmi_op global;                 /* HEAD_GLOBAL: DENSE, ASHAPE, VSLASH or GRID */
+  mmi_op intra[MMI_MAX_MODALITIES];
+  /* QBOUNDARY: intra[m] in DENSE, ASHAPE, VSLASH (global positions).
+   * 2D: intra[m] in DENSE, ASHAPE, VSLASH, GRID (modality-local coordinates). */
+  mmi_op cross[MMI_MAX_MODALITIES][MMI_MAX_MODALITIES];
+  /* 2D: cross[mq][mk], mq != mk, in NONE, DENSE, VERT. */
+} mmi_head_cfg;
+
+typedef struct mmi_problem {
+  int64_t S;                     /* tokens, 1 <= S <= MMI_MAX_SEQ */
+  int32_t Hq, Hkv;               /* query / KV heads, Hq % Hkv == 0 */
+  int32_t D;                     /* must be 128 */
+  int32_t block;                 /* must be 64 */
+  int64_t q_stride_s, q_stride_h;  /* element strides; 0,0 = packed [S,Hq,128] */
+  int64_t k_stride_s, k_stride_h;  /* packed [S,Hkv,128] */
+  int64_t v_stride_s, v_stride_h;
+  int64_t o_stride_s, o_stride_h;  /* packed [S,Hq,128] */
+  const uint8_t* modality;       /* HOST array [S] of modality ids < n_modalities, or NULL */
+  int32_t n_modalities;          /* 1..MMI_MAX_MODALITIES (ignored if modality == NULL) */
+} mmi_problem;
+
+typedef struct mmi_ctx mmi_ctx;
+typedef struct mmi_plan mmi_plan;
+
+typedef struct mmi_head_stats {
+  int32_t kind;                  /* head kind */
+  int32_t n_qblocks, n_kblocks;  /* permuted query / key blocks (incl. padding) */
+  int64_t nnz_blocks;            /* selected (query block, key block) pairs */
+  int64_t causal_blocks;         /* query-block x key-block pairs with a causal element */
+  int32_t split_rows;            /* query blocks split across work items */
+  int32_t sigma[MMI_MAX_MODALITIES];  /* chosen Grid stride per op slot (0 = not Grid / dense fallback) */
+  int32_t phase[MMI_MAX_MODALITIES];
+} mmi_head_stats;
+
+/* export kinds for mmi_plan_export (host copies; the call synchronises) */
+#define MMI_EXPORT_QPERM 0       /* int32[n_qblocks*64]: slot -> position or -1 */
+#define MMI_EXPORT_KPERM 1       /* int32[n_kblocks*64] */
+#define MMI_EXPORT_ROW_PTR 2     /* int32[n_qblocks+1] */
+#define MMI_EXPORT_COL_IDX 3     /* int32[nnz_blocks], ascending within a row */
+#define MMI_EXPORT_V_SCORES 4    /* float[L_c]: column scores of the estimate */
+#define MMI_EXPORT_U_SCORES 5    /* float[L_c]: diagonal scores */
+#define MMI_EXPORT_FOLD 6        /* float[(hi-lo+1)*1024]: Grid fold c_s[p] at [s-lo][p] */
+#define MMI_EXPORT_VSEL 7        /* int32[n]: selected vertical coordinates, ascending */
+#define MMI_EXPORT_SSEL 8        /* int32[n]: selected slash offsets, ascending */
+#define MMI_EXPORT_PARAMS 9      /* int32[4]: {sigma, phase, L_c, n_rows} (sigma 0 = dense) */
+#define MMI_EXPORT_EST_LSE 10    /* float[n_rows]: natural-log LSE of the estimation rows */
+
+int mmi_version(void);
+const char* mmi_status_str(int status);   /* static string, never NULL */
+const char* mmi_last_error(void);         /* thread-local detail of the last error */
+
+/* Context: binds a device, owns a cache of device workspace. */
+int mmi_ctx_create(int device, mmi_ctx** out);
+int mmi_ctx_destroy(mmi_ctx* ctx);
+
+/* Estimation, choices, permutations and block index of every head
+ * (Algorithms 1-3 up to the kernel launch). Enqueued on `stream`; the call
+ * synchronises once with it (to size the block index). q, k: device
+ * tensors described by `prob`; cfgs: host array [Hq]. Block (i, j) is
+ * selected iff some query of permuted query block i and key of permuted key
+ * block j satisfy k <= q in original positions and the head's predicate, or
+ * block j holds the diagonal key of one of block i's queries. The plan owns
+ * its device buffers until mmi_plan_destroy. */
+int mmi_plan_create(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* cfgs,
+                    const void* q, const void* k, void* stream, mmi_plan** out);
+
+/* Block-sparse causal attention over the plan (Algorithms 5-7): gathers
+ * permuted Q/K/V rows inside the kernel, online softmax in fp32, P rounded
+ * to bf16 for the PV product, O written as bf16 (round to nearest even) in
+ * original token order. lse: device float [Hq][S] natural-log LSE, or NULL. */
+int mmi_plan_execute(mmi_plan* plan, const void* q, const void* k, const void* v,
+                     void* o, float* lse, void* stream);
+
+int mmi_plan_stats(mmi_plan* plan, int head, mmi_head_stats* out);
+
+/* Copy one plan array of `head` to host memory. slot selects the op:
+ * 0 for a global head, m for modality m (QBOUNDARY / 2D intra), and
+ * 8 + mq*8 + mk for a 2D cross pair. If host_dst is NULL or bytes is too
+ * small, only *needed is written (and MMI_OK returned if dst is NULL). */
+int mmi_plan_export(mmi_plan* plan, int head, int what, int slot, void* host_dst,
+                    size_t bytes, size_t* needed);
+
+int mmi_plan_destroy(mmi_plan* plan);
+
+/* create + execute + destroy. */
+int mmi_attention(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* cfgs,
+                  const void* q, const void* k, const void* v, void* o, float* lse,
+                  void* stream);
+
+/* Every causal block of every head through the same kernel: the dense
+ * causal attention baseline on the same GPU. */
+int mmi_dense_attention(mmi_ctx* ctx, const mmi_problem* prob, const void* q,
+                        const void* k, const void* v, void* o, float* lse, void* stream);
+
+/* Explicit row permutation (the Q/K/V permutation of Algorithms 1-3 done as
+ * a separate pass): dst row x = src row perm[x] (perm[x] = -1 -> zero row),
+ * for x in [0, n_dst). unpermute: dst row perm[x] = src row x for perm[x] >= 0.
+ * Rows are row_bytes long (multiple of 16), strides in bytes, perm is a
+ * device int32 array. */
+int mmi_permute_rows(const void* src, int64_t src_stride, void* dst, int64_t dst_stride,
+                     const int32_t* perm, int64_t n_dst, int64_t row_bytes, void* stream);
+int mmi_unpermute_rows(const void* src, int64_t src_stride, void* dst, int64_t dst_stride,
+                       const int32_t* perm, int64_t n_src, int64_t row_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MMI_H */

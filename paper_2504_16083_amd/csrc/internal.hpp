@@ -1,0 +1,167 @@
+// Internal device-side descriptors and launch entry points of libmmi.
+// Host C++ (runtime.hip) fills these records; the kernels in k_*.hip read
+// them. Nothing here is part of the public C-ABI (include/mmi.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/mmi.h"
+
+namespace mmi {
+
+constexpr int B = 64;            // block size (rows and keys)
+constexpr int D = 128;           // head dim
+constexpr int LASTQ = 64;        // estimation rows
+constexpr int FOLD_W = 1024;     // fold row width (max stride)
+constexpr int INT_BIG = 0x7fffffff;
+
+// Tensor view: element strides, head dim contiguous.
+struct Tensor {
+  const void* p;
+  int64_t ss, sh;
+};
+
+// ---------------------------------------------------------------- layout
+struct Segment {      // maximal run of one modality
+  int32_t pos;        // first position
+  int32_t len;
+  int32_t loc;        // index of `pos` inside its modality's position list
+  int32_t mod;
+};
+
+// ---------------------------------------------------------------- estimation
+struct RowSet {       // estimation query rows: positions [row0, row0 + nrows)
+  int32_t head, kvh, row0, nrows;
+  int32_t nchunks;    // key chunks of pass 1
+  float* part;        // [nchunks][64][2] (max, sum) in log2 domain
+  float* lse2;        // [64] log2-domain LSE
+};
+
+struct EstJob {       // one query set x one key coordinate system
+  int32_t head, kvh, row0, nrows, rowset;
+  int32_t coord0;     // coordinate of row0 in the key system (u only)
+  const int32_t* keymap;  // coordinate -> position, nullptr = identity
+  int32_t L_c, ntiles;
+  float* v;           // [L_c]
+  float* u;           // [L_c] or nullptr
+  float* dpart;       // [ntiles][128] or nullptr
+};
+
+struct GridJob {      // stride search over one job's v
+  const float* v;
+  int32_t L_c, lo, hi;   // candidate strides after the 2*s <= L_c cut (hi < lo: none)
+  float* fold;        // [hi-lo+1][1024]
+  float* score;       // [hi-lo+1]
+  int32_t* pick;      // [hi-lo+1] phase of the max
+  int32_t* params;    // [4] out: sigma (0 = dense), phase, L_c, nrows
+  int32_t nrows;
+};
+
+struct TopkJob {
+  const float* x;
+  int32_t L, n;       // n <= L
+  int32_t* out;       // [n] ascending
+};
+
+// ---------------------------------------------------------------- plan
+struct OpDev {
+  int32_t kind;               // MMI_OP_* (GRID may fall back to dense via params)
+  int32_t sink, local;
+  int32_t use_h, use_v, use_s;
+  int32_t L;                  // extent of the op's coordinate system
+  int32_t kbase, nkblk;       // first key block / number of key blocks of the key group
+  const int32_t* params;      // GRID: {sigma, phase}
+  const int32_t* vsel; int32_t nv;
+  const int32_t* ssel; int32_t ns;
+  int32_t* minsel;            // [nkblk] smallest selected key position per key block
+  const int32_t* keymap;      // coordinate -> position for VSLASH/VERT (nullptr = identity)
+  int32_t kgrid;              // key group is Grid-ordered (VERT into a Grid group)
+  const int32_t* kparams;     // that group's {sigma, phase}
+  int32_t koff;               // key group slot offset
+};
+
+struct HeadDev {
+  int32_t kind, kvh;
+  int32_t nbq, nbk;           // permuted query / key blocks
+  int32_t S;
+  int32_t* qperm;             // [nbq*64] or nullptr (identity)
+  int32_t* kperm;             // [nbk*64] or nullptr (identity)
+  int32_t* kminpos;           // [nbk] smallest key position per key block
+  int32_t* counts;            // [nbq]
+  int32_t* rowptr;            // [nbq+1]
+  uint32_t* bitmap;           // [nbq][nwords]
+  int32_t nwords;
+  int32_t* col;               // [nnz]
+  int32_t op0;                // first OpDev of this head
+  int32_t* chunks;            // [nbq] work items per row
+  int32_t* itembase;          // [nbq] exclusive prefix of chunks
+  int32_t* splitoff;          // [nbq] exclusive prefix of (chunks > 1)
+  int32_t* partoff;           // [nbq] exclusive prefix of chunks over split rows
+};
+
+// group table (modalities present, ascending); identical for every boundary head
+struct Groups {
+  int32_t n;
+  int32_t mod[MMI_MAX_MODALITIES];
+  int32_t off[MMI_MAX_MODALITIES];    // slot offset (multiple of 64)
+  int32_t len[MMI_MAX_MODALITIES];    // |T_m|
+  int32_t toff[MMI_MAX_MODALITIES];   // offset of T_m inside the position pool
+};
+
+struct WorkItem {
+  int32_t head, qblk, e0, e1;
+  int32_t part;       // -1: write O directly; else partial slot
+  int32_t pad[3];
+};
+
+struct SplitRow {
+  int32_t head, qblk, part0, nparts;
+};
+
+// ---------------------------------------------------------------- launches
+// k_layout.hip
+hipError_t launch_positions(const Segment* segs, int nseg, const int32_t* toff_by_mod, int32_t* tpos,
+                            int S, hipStream_t st);
+hipError_t launch_perms(const HeadDev* heads, int nheads, const OpDev* ops, Groups g,
+                        const int32_t* tpos, int S, int max_nbq_slots, hipStream_t st);
+// k_estimate.hip
+hipError_t launch_est_lse(const RowSet* rs, int nrs, int max_chunks, Tensor q, Tensor k,
+                          int chunk_keys, hipStream_t st);
+hipError_t launch_est_scores(const EstJob* jobs, int njobs, int max_tiles, const RowSet* rs,
+                             Tensor q, Tensor k, hipStream_t st);
+hipError_t launch_est_udiag(const EstJob* jobs, int njobs, int max_L, hipStream_t st);
+// k_select.hip
+hipError_t launch_grid_search(const GridJob* jobs, int njobs, int max_cands, hipStream_t st);
+hipError_t launch_topk(const TopkJob* jobs, int njobs, hipStream_t st);
+// k_blocks.hip
+hipError_t launch_key_summaries(const HeadDev* heads, int nheads, OpDev* ops, int nops,
+                                Groups g, int max_nbk, int max_sel, hipStream_t st);
+hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* ops, Groups g,
+                               const int32_t* tpos, const Segment* segs, int nseg, int max_nbq,
+                               int chunk_blocks, hipStream_t st);
+// totals[head] = {nnz, nitems, nsplit, nparts}
+hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int64_t* totals, hipStream_t st);
+hipError_t launch_blocks_fill(const HeadDev* heads, int nheads, int max_nbq, hipStream_t st);
+hipError_t launch_work_fill(const HeadDev* heads, int nheads, const int64_t* item_base,
+                            const int64_t* part_base, const int64_t* split_base, int max_nbq,
+                            int chunk_blocks, WorkItem* items, SplitRow* splits, hipStream_t st);
+// k_attention.hip
+struct AttnArgs {
+  Tensor q, k, v;
+  void* o; int64_t o_ss, o_sh;
+  float* lse;                 // [Hq][S] or nullptr
+  int32_t S;
+  const HeadDev* heads;
+  const WorkItem* items;
+  int64_t nitems;
+  float* part_o;              // [nparts][64][128]
+  float* part_ml;             // [nparts][64][2]
+};
+hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
+hipError_t launch_combine(const AttnArgs& a, const SplitRow* splits, int64_t nsplit, hipStream_t st);
+// k_permute.hip
+hipError_t launch_permute(const void* src, int64_t ss, void* dst, int64_t ds, const int32_t* perm,
+                          int64_t n, int64_t row_bytes, int inverse, hipStream_t st);
+
+}  // namespace mmi

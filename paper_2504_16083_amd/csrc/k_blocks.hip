@@ -1,0 +1,383 @@
+// Block-index construction: the causal block lift of every head's token
+// predicate ("sparse loading, dense computation": whole 64x64 blocks are
+// loaded and computed), plus the key block holding each query's own key.
+// The mask-index building of the 2D-Boundary head (Section 3.2) and the
+// vertical/slash -> block conversion of the VS head (Appendix C.3) are the
+// same operation here.
+//
+// k_key_summaries: per key block the smallest key position (kminpos) and,
+//   per VS / VERT op, the smallest selected key position (minsel).
+// k_blocks_count: one workgroup per (head, query block) sets the selected key
+//   blocks in an LDS bitmap with closed-form rules (ranges, per-block
+//   threshold tests, slash offsets), then stores the bitmap and its
+//   popcount. Bit setting is an OR, so the result is order independent.
+// k_blocks_scan: per head, prefix sums of counts (CSR row pointers) and of
+//   work-item counts.
+// k_blocks_fill: ascending column lists from the bitmaps.
+// k_work_fill: work items (a query block and <= chunk key blocks each) and
+//   the split-row table for the combine kernel.
+#include "device.hpp"
+#include "internal.hpp"
+
+namespace mmi {
+
+__global__ __launch_bounds__(256) void k_kminpos(const HeadDev* heads) {
+  const HeadDev hd = heads[blockIdx.x];
+  const int j = blockIdx.y * 256 + threadIdx.x;
+  if (!hd.kminpos || j >= hd.nbk) return;
+  int mn = INT_BIG;
+  for (int x = 0; x < B; ++x) {
+    const int slot = j * B + x;
+    const int p = hd.kperm ? hd.kperm[slot] : (slot < hd.S ? slot : -1);
+    if (p >= 0) mn = min(mn, p);
+  }
+  hd.kminpos[j] = mn;
+}
+
+__global__ __launch_bounds__(256) void k_minsel_init(OpDev* ops) {
+  const OpDev op = ops[blockIdx.x];
+  const int j = blockIdx.y * 256 + threadIdx.x;
+  if (op.minsel && j < op.nkblk) op.minsel[j] = INT_BIG;
+}
+
+__global__ __launch_bounds__(256) void k_minsel_scatter(OpDev* ops) {
+  const OpDev op = ops[blockIdx.x];
+  const int i = blockIdx.y * 256 + threadIdx.x;
+  if (!op.minsel || i >= op.nv) return;
+  const int kap = op.vsel[i];
+  const int pos = op.keymap ? op.keymap[kap] : kap;
+  int local = kap;
+  if (op.kgrid && op.kparams[0] > 0) local = grid_slot(grid_geo(op.L, op.kparams[0], op.kparams[1]), kap);
+  atomicMin(&op.minsel[local / B], pos);
+}
+
+hipError_t launch_key_summaries(const HeadDev* heads, int nheads, OpDev* ops, int nops, Groups g,
+                                int max_nbk, int max_sel, hipStream_t st) {
+  (void)g;
+  if (nheads > 0 && max_nbk > 0)
+    hipLaunchKernelGGL(k_kminpos, dim3(nheads, (max_nbk + 255) / 256), dim3(256), 0, st, heads);
+  if (nops > 0 && max_nbk > 0)
+    hipLaunchKernelGGL(k_minsel_init, dim3(nops, (max_nbk + 255) / 256), dim3(256), 0, st, ops);
+  if (nops > 0 && max_sel > 0)
+    hipLaunchKernelGGL(k_minsel_scatter, dim3(nops, (max_sel + 255) / 256), dim3(256), 0, st, ops);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- bitmap rules
+struct RowInfo {
+  int nvalid;        // valid rows (a prefix of the block)
+  int maxpos;        // largest original position among the rows
+  int nruns;         // runs of consecutive coordinates
+};
+
+__device__ __forceinline__ void set_bit(uint32_t* bm, int j) { atomicOr(&bm[j >> 5], 1u << (j & 31)); }
+
+// all threads call with the same (a, b)
+__device__ __forceinline__ void set_range(uint32_t* bm, int a, int b) {
+  if (b < a) return;
+  const int w0 = a >> 5, w1 = b >> 5;
+  for (int w = w0 + (int)threadIdx.x; w <= w1; w += blockDim.x) {
+    uint32_t m = 0xffffffffu;
+    if (w == w0) m &= 0xffffffffu << (a & 31);
+    if (w == w1) m &= 0xffffffffu >> (31 - (b & 31));
+    atomicOr(&bm[w], m);
+  }
+}
+
+// key blocks [kbase, kbase + n) whose threshold value thr[j - kbase] <= lim
+__device__ __forceinline__ void set_threshold(uint32_t* bm, const int32_t* thr, int kbase, int n, int lim,
+                                              bool identity_blocks) {
+  for (int jj = threadIdx.x; jj < n; jj += blockDim.x) {
+    const int t = identity_blocks ? (kbase + jj) * B : thr[jj];
+    if (t <= lim) set_bit(bm, kbase + jj);
+  }
+}
+
+// dense / A-shape / VS over coordinates whose keys sit at key block kbase + c / 64
+__device__ void identity_rules(uint32_t* bm, const OpDev& op, const int* ra, const int* rb, int nruns,
+                               int maxpos, int kbase) {
+  const int qmax = rb[nruns - 1];
+  if (op.kind == MMI_OP_DENSE || (op.kind == MMI_OP_GRID)) {   // GRID here = dense fallback
+    set_range(bm, kbase, kbase + qmax / B);
+  } else if (op.kind == MMI_OP_ASHAPE) {
+    if (op.sink > 0) set_range(bm, kbase, kbase + min(op.sink - 1, qmax) / B);
+    if (op.local > 0)
+      for (int r = 0; r < nruns; ++r) set_range(bm, kbase + max(0, ra[r] - op.local + 1) / B, kbase + rb[r] / B);
+  } else if (op.kind == MMI_OP_VSLASH) {
+    set_threshold(bm, op.minsel, kbase, op.nkblk, maxpos, false);
+    for (int idx = threadIdx.x; idx < op.ns; idx += blockDim.x) {
+      const int o = op.ssel[idx];
+      for (int r = 0; r < nruns; ++r) {
+        if (rb[r] < o) continue;
+        const int lo = max(0, ra[r] - o) / B, hi = (rb[r] - o) / B;
+        for (int j = lo; j <= hi; ++j) set_bit(bm, kbase + j);
+      }
+    }
+  }
+}
+
+// Grid closed forms in the slot space [0, L) of one group (key blocks kbase + ...)
+__device__ void grid_rules(uint32_t* bm, const OpDev& op, int sig, int ph, int L, int il, int kbase,
+                           const int* rpos, const int32_t* kminpos, bool identity_k, int* sh_maxc) {
+  const GridGeo geo = grid_geo(L, sig, ph);
+  const int lo = il * B, hi = min(lo + B, L) - 1;
+  if (threadIdx.x == 0) *sh_maxc = -1;
+  __syncthreads();
+  if ((int)threadIdx.x <= hi - lo) atomicMax(sh_maxc, grid_coord(geo, lo + threadIdx.x));
+  __syncthreads();
+  const int maxc = *sh_maxc;
+  const int g0p = grid_g0(geo, ph);
+  if (op.use_s) {
+    const int cf = grid_coord(geo, lo);
+    set_range(bm, kbase + grid_g0(geo, cf % sig) / B, kbase + il);
+  }
+  if (op.use_v && maxc >= ph) {
+    const int f = (maxc - ph) / sig;
+    set_range(bm, kbase + g0p / B, kbase + (g0p + f) / B);
+  }
+  if (op.use_h && hi >= g0p) {
+    const int qh = rpos[hi - lo];
+    set_threshold(bm, kminpos + kbase, kbase, (L + B - 1) / B, qh, identity_k);
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(256) void k_blocks_count(const HeadDev* heads, const OpDev* ops, Groups g,
+                                                      int chunk) {
+  const HeadDev hd = heads[blockIdx.x];
+  const int qb = blockIdx.y;
+  if (qb >= hd.nbq) return;
+  __shared__ uint32_t bm[MMI_MAX_SEQ / B / 32 + 8];   // + one block per padded group
+  __shared__ int rpos[B], rc[B], ra[B], rb[B];
+  __shared__ int sh_nvalid, sh_maxpos, sh_nruns, sh_count, sh_maxc;
+  const int tid = threadIdx.x;
+  for (int w = tid; w < hd.nwords; w += blockDim.x) bm[w] = 0;
+  int gi = -1, li0 = 0;
+  if (hd.kind != MMI_HEAD_GLOBAL) {
+    const int x = qb * B;
+    for (int i = 0; i < g.n; ++i) {
+      const int padded = (g.len[i] + B - 1) / B * B;
+      if (x >= g.off[i] && x < g.off[i] + padded) gi = i;
+    }
+    if (gi < 0) return;      // not reachable: every slot < nbq*64 lies in a group
+    li0 = x - g.off[gi];
+  }
+  if (tid < B) {
+    const int slot = qb * B + tid;
+    const int p = hd.qperm ? hd.qperm[slot] : (slot < hd.S ? slot : -1);
+    rpos[tid] = p;
+    rc[tid] = hd.kind == MMI_HEAD_2D ? li0 + tid : p;   // coordinate of the row for identity-order rules
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int nv = 0, mp = -1, nr = 0;
+    for (int r = 0; r < B; ++r) {
+      if (rpos[r] < 0) break;
+      ++nv;
+      mp = max(mp, rpos[r]);
+      if (nr > 0 && rc[r] == rb[nr - 1] + 1) {
+        rb[nr - 1] = rc[r];
+      } else {
+        ra[nr] = rc[r];
+        rb[nr] = rc[r];
+        ++nr;
+      }
+    }
+    sh_nvalid = nv;
+    sh_maxpos = mp;
+    sh_nruns = nr;
+    sh_count = 0;
+  }
+  __syncthreads();
+  const int maxpos = sh_maxpos, nruns = sh_nruns;
+  if (hd.kind == MMI_HEAD_GLOBAL) {
+    const OpDev op = ops[hd.op0];
+    const int sig = op.kind == MMI_OP_GRID ? op.params[0] : 0;
+    if (sig > 0)
+      grid_rules(bm, op, sig, op.params[1], hd.S, qb, 0, rpos, hd.kminpos, false, &sh_maxc);
+    else
+      identity_rules(bm, op, ra, rb, nruns, maxpos, 0);
+    if (tid == 0) set_bit(bm, qb);
+  } else if (hd.kind == MMI_HEAD_QBOUNDARY) {
+    const OpDev op = ops[hd.op0 + gi];
+    identity_rules(bm, op, ra, rb, nruns, maxpos, 0);
+    for (int r = 0; r < nruns; ++r) set_range(bm, ra[r] / B, rb[r] / B);
+  } else {
+    for (int gk = 0; gk < g.n; ++gk) {
+      const OpDev op = ops[hd.op0 + gi * g.n + gk];
+      const int kbase = g.off[gk] / B;
+      const int nk = (g.len[gk] + B - 1) / B;
+      if (gk == gi) {
+        const int sig = op.kind == MMI_OP_GRID ? op.params[0] : 0;
+        if (sig > 0)
+          grid_rules(bm, op, sig, op.params[1], g.len[gi], li0 / B, kbase, rpos, hd.kminpos, false, &sh_maxc);
+        else
+          identity_rules(bm, op, ra, rb, nruns, maxpos, kbase);
+      } else if (op.kind == MMI_OP_DENSE) {
+        set_threshold(bm, hd.kminpos + kbase, kbase, nk, maxpos, false);
+      } else if (op.kind == MMI_OP_VERT) {
+        set_threshold(bm, op.minsel, kbase, nk, maxpos, false);
+      }
+    }
+    if (tid == 0) set_bit(bm, qb);
+  }
+  __syncthreads();
+  int cnt = 0;
+  uint32_t* gbm = hd.bitmap + (int64_t)qb * hd.nwords;
+  for (int w = tid; w < hd.nwords; w += blockDim.x) {
+    const uint32_t v = bm[w];
+    gbm[w] = v;
+    cnt += __popc(v);
+  }
+  atomicAdd(&sh_count, cnt);
+  __syncthreads();
+  if (tid == 0) {
+    hd.counts[qb] = sh_count;
+    hd.chunks[qb] = (sh_count + chunk - 1) / chunk;
+  }
+}
+
+hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* ops, Groups g,
+                               const int32_t* tpos, const Segment* segs, int nseg, int max_nbq, int chunk,
+                               hipStream_t st) {
+  (void)tpos; (void)segs; (void)nseg;
+  if (nheads <= 0 || max_nbq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_blocks_count, dim3(nheads, max_nbq), dim3(256), 0, st, heads, ops, g, chunk);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- scans
+constexpr int SCAN_T = 1024;
+
+// exclusive block scan of one int per thread; returns the block total
+__device__ int block_exscan(int v, int* buf, int& excl) {
+  const int tid = threadIdx.x;
+  buf[tid] = v;
+  __syncthreads();
+  for (int off = 1; off < SCAN_T; off <<= 1) {
+    const int t = tid >= off ? buf[tid - off] : 0;
+    __syncthreads();
+    buf[tid] += t;
+    __syncthreads();
+  }
+  excl = buf[tid] - v;
+  const int tot = buf[SCAN_T - 1];
+  __syncthreads();
+  return tot;
+}
+
+__global__ __launch_bounds__(SCAN_T) void k_blocks_scan(const HeadDev* heads, int64_t* totals) {
+  const HeadDev hd = heads[blockIdx.x];
+  __shared__ int buf[SCAN_T];
+  int c_nnz = 0, c_items = 0, c_split = 0, c_parts = 0;
+  for (int start = 0; start < hd.nbq; start += SCAN_T) {
+    const int i = start + threadIdx.x;
+    const int cnt = i < hd.nbq ? hd.counts[i] : 0;
+    const int ch = i < hd.nbq ? hd.chunks[i] : 0;
+    const int sp = ch > 1 ? 1 : 0;
+    const int pt = ch > 1 ? ch : 0;
+    int e0, e1, e2, e3;
+    const int t0 = block_exscan(cnt, buf, e0);
+    const int t1 = block_exscan(ch, buf, e1);
+    const int t2 = block_exscan(sp, buf, e2);
+    const int t3 = block_exscan(pt, buf, e3);
+    if (i < hd.nbq) {
+      hd.rowptr[i] = c_nnz + e0;
+      hd.itembase[i] = c_items + e1;
+      hd.splitoff[i] = c_split + e2;
+      hd.partoff[i] = c_parts + e3;
+    }
+    c_nnz += t0; c_items += t1; c_split += t2; c_parts += t3;
+  }
+  if (threadIdx.x == 0) {
+    hd.rowptr[hd.nbq] = c_nnz;
+    totals[blockIdx.x * 4 + 0] = c_nnz;
+    totals[blockIdx.x * 4 + 1] = c_items;
+    totals[blockIdx.x * 4 + 2] = c_split;
+    totals[blockIdx.x * 4 + 3] = c_parts;
+  }
+}
+
+hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int64_t* totals, hipStream_t st) {
+  if (nheads <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_blocks_scan, dim3(nheads), dim3(SCAN_T), 0, st, heads, totals);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void k_blocks_fill(const HeadDev* heads) {
+  const HeadDev hd = heads[blockIdx.x];
+  const int qb = blockIdx.y;
+  if (qb >= hd.nbq) return;
+  __shared__ int buf[256];
+  const uint32_t* gbm = hd.bitmap + (int64_t)qb * hd.nwords;
+  const int per = (hd.nwords + 255) / 256;
+  const int w0 = threadIdx.x * per;
+  int cnt = 0;
+  for (int w = w0; w < min(w0 + per, hd.nwords); ++w) cnt += __popc(gbm[w]);
+  buf[threadIdx.x] = cnt;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int t = threadIdx.x >= off ? buf[threadIdx.x - off] : 0;
+    __syncthreads();
+    buf[threadIdx.x] += t;
+    __syncthreads();
+  }
+  int pos = hd.rowptr[qb] + buf[threadIdx.x] - cnt;
+  for (int w = w0; w < min(w0 + per, hd.nwords); ++w) {
+    uint32_t v = gbm[w];
+    while (v) {
+      const int b = __ffs(v) - 1;
+      hd.col[pos++] = w * 32 + b;
+      v &= v - 1;
+    }
+  }
+}
+
+hipError_t launch_blocks_fill(const HeadDev* heads, int nheads, int max_nbq, hipStream_t st) {
+  if (nheads <= 0 || max_nbq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_blocks_fill, dim3(nheads, max_nbq), dim3(256), 0, st, heads);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void k_work_fill(const HeadDev* heads, const int64_t* item_base,
+                                                   const int64_t* part_base, const int64_t* split_base,
+                                                   int chunk, WorkItem* items, SplitRow* splits) {
+  const int h = blockIdx.x;
+  const HeadDev hd = heads[h];
+  const int qb = blockIdx.y * 256 + threadIdx.x;
+  if (qb >= hd.nbq) return;
+  const int nch = hd.chunks[qb];
+  const int r0 = hd.rowptr[qb], r1 = hd.rowptr[qb + 1];
+  const int64_t ib = item_base[h] + hd.itembase[qb];
+  const bool split = nch > 1;
+  const int64_t pb = part_base[h] + hd.partoff[qb];
+  for (int c = 0; c < nch; ++c) {
+    WorkItem w;
+    w.head = h;
+    w.qblk = qb;
+    w.e0 = r0 + c * chunk;
+    w.e1 = min(r0 + (c + 1) * chunk, r1);
+    w.part = split ? (int)(pb + c) : -1;
+    w.pad[0] = w.pad[1] = w.pad[2] = 0;
+    items[ib + c] = w;
+  }
+  if (split) {
+    SplitRow s;
+    s.head = h;
+    s.qblk = qb;
+    s.part0 = (int)pb;
+    s.nparts = nch;
+    splits[split_base[h] + hd.splitoff[qb]] = s;
+  }
+}
+
+hipError_t launch_work_fill(const HeadDev* heads, int nheads, const int64_t* item_base,
+                            const int64_t* part_base, const int64_t* split_base, int max_nbq, int chunk,
+                            WorkItem* items, SplitRow* splits, hipStream_t st) {
+  if (nheads <= 0 || max_nbq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_work_fill, dim3(nheads, (max_nbq + 255) / 256), dim3(256), 0, st, heads, item_base,
+                     part_base, split_base, chunk, items, splits);
+  return hipGetLastError();
+}
+
+}  // namespace mmi

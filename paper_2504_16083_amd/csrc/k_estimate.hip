@@ -1,0 +1,206 @@
+// Online estimate of the attention map from the final queries (Algorithm 1,
+// first step; Appendix C.3): A_hat[r, k] = exp(tau q_r.k_k - LSE_r) for
+// k <= pos(r), each row normalised over all causal keys of the sequence.
+//
+// Pass 1 (k_est_lse): per query set and key chunk, running (max, sum) of
+//   2^(tau log2e q.k) per row -> partials; k_est_merge folds the chunks in
+//   a fixed order into log2-domain LSE.
+// Pass 2 (k_est_scores): per query set and 64-key tile of the key
+//   coordinate system, A_hat tile through MFMA, then in LDS the column sums
+//   (v, written directly: each tile owns its keys) and the 127 diagonal
+//   partial sums of the tile; k_est_udiag adds the (at most two) tiles that
+//   touch each diagonal offset. Every reduction has a fixed order, so the
+//   scores are bitwise reproducible.
+// The query rows are contiguous positions [row0, row0+nrows), nrows <= 64,
+// and contiguous in the key coordinate system too (coordinate coord0 + r).
+// K rows are read straight from HBM into MFMA operands (each lane loads one
+// contiguous 128-byte half row); no LDS staging is needed for S^T = K Q^T.
+#include "device.hpp"
+#include "internal.hpp"
+
+namespace mmi {
+
+namespace {
+
+constexpr float SC = 0.08838834764831845f * LOG2E;   // sqrt(1/128) * log2(e)
+
+__device__ __forceinline__ void load_q_operand(bf16x8 (&qr)[8], const Tensor& q, int head, int pos,
+                                               int h) {
+  const uint16_t* row = reinterpret_cast<const uint16_t*>(q.p) + (int64_t)head * q.sh +
+                        (int64_t)max(pos, 0) * q.ss + h * 64;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) qr[s] = pos >= 0 ? load16(row + 8 * s) : zero8();
+}
+
+// S^T tile of 32 keys x 32 queries; lane (c, h) holds keys 8i + 4h + j for query c.
+__device__ __forceinline__ f32x16 key_tile(const Tensor& k, int kvh, int kpos, int h,
+                                           const bf16x8 (&qr)[8]) {
+  const uint16_t* row = reinterpret_cast<const uint16_t*>(k.p) + (int64_t)kvh * k.sh +
+                        (int64_t)max(kpos, 0) * k.ss + h * 64;
+  bf16x8 ka[8];
+#pragma unroll
+  for (int s = 0; s < 8; ++s) ka[s] = kpos >= 0 ? load16(row + 8 * s) : zero8();
+  f32x16 acc;
+#pragma unroll
+  for (int x = 0; x < 16; ++x) acc[x] = 0.0f;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) acc = mfma32(ka[s], qr[s], acc);
+  return acc;
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(128) void k_est_lse(const RowSet* sets, Tensor q, Tensor k, int chunk_keys) {
+  const RowSet rs = sets[blockIdx.x];
+  const int ch = blockIdx.y;
+  if (ch >= rs.nchunks) return;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
+  const int r = wave * 32 + c;
+  const int qpos = r < rs.nrows ? rs.row0 + r : -1;
+  bf16x8 qr[8];
+  load_q_operand(qr, q, rs.head, qpos, h);
+  const int limit = rs.row0 + rs.nrows;           // keys [0, limit) can be visible
+  const int k0 = ch * chunk_keys;
+  const int k1 = min(k0 + chunk_keys, limit);
+  float m = NEG_BIG, l = 0.0f;
+  for (int kb = k0; kb < k1; kb += 32) {
+    const int kp = kb + c < k1 ? kb + c : -1;
+    const f32x16 s = key_tile(k, rs.kvh, kp, h, qr);
+    float mx = NEG_BIG;
+    float x[16];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int key = kb + 8 * i + 4 * h + j;
+        const float v = s[4 * i + j] * SC;
+        x[4 * i + j] = (key < k1 && key <= qpos) ? v : -INFINITY;
+        mx = fmaxf(mx, x[4 * i + j]);
+      }
+    const float mn = fmaxf(m, mx);
+    float acc = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc += fast_exp2(x[e] - mn);
+    l = l * fast_exp2(m - mn) + acc;
+    m = mn;
+  }
+  const float m2 = __shfl_xor(m, 32), l2 = __shfl_xor(l, 32);
+  const float mt = fmaxf(m, m2);
+  const float lt = h == 0 ? l * fast_exp2(m - mt) + l2 * fast_exp2(m2 - mt)
+                          : l2 * fast_exp2(m2 - mt) + l * fast_exp2(m - mt);
+  if (h == 0) {
+    float* p = rs.part + ((int64_t)ch * LASTQ + r) * 2;
+    p[0] = mt;
+    p[1] = lt;
+  }
+}
+
+__global__ __launch_bounds__(64) void k_est_merge(const RowSet* sets) {
+  const RowSet rs = sets[blockIdx.x];
+  const int r = threadIdx.x;
+  if (r >= rs.nrows) return;
+  float M = NEG_BIG;
+  for (int ch = 0; ch < rs.nchunks; ++ch) M = fmaxf(M, rs.part[((int64_t)ch * LASTQ + r) * 2]);
+  float L = 0.0f;
+  for (int ch = 0; ch < rs.nchunks; ++ch) {
+    const float* p = rs.part + ((int64_t)ch * LASTQ + r) * 2;
+    L += p[1] * fast_exp2(p[0] - M);
+  }
+  rs.lse2[r] = M + fast_log2(L);
+}
+
+constexpr int APITCH = 65;
+
+__global__ __launch_bounds__(128) void k_est_scores(const EstJob* jobs, const RowSet* sets, Tensor q,
+                                                    Tensor k) {
+  __shared__ float ahat[B * APITCH];
+  const EstJob jb = jobs[blockIdx.x];
+  const int t = blockIdx.y;
+  if (t >= jb.ntiles) return;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
+  const int r = wave * 32 + c;
+  const int qpos = r < jb.nrows ? jb.row0 + r : -1;
+  const float lse2 = qpos >= 0 ? sets[jb.rowset].lse2[r] : 0.0f;
+  bf16x8 qr[8];
+  load_q_operand(qr, q, jb.head, qpos, h);
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) {
+    const int kap = t * B + kt * 32 + c;          // coordinate loaded by this lane
+    const int kp = kap < jb.L_c ? (jb.keymap ? jb.keymap[kap] : kap) : -1;
+    const f32x16 s = key_tile(k, jb.kvh, kp, h, qr);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int kk = kt * 32 + 8 * i + 4 * h + j;   // key index inside the tile
+        const int kap2 = t * B + kk;
+        const int kp2 = kap2 < jb.L_c ? (jb.keymap ? jb.keymap[kap2] : kap2) : INT_BIG;
+        const float a = (qpos >= 0 && kp2 <= qpos) ? fast_exp2(s[4 * i + j] * SC - lse2) : 0.0f;
+        ahat[kk * APITCH + r] = a;
+      }
+  }
+  __syncthreads();
+  {   // column sums: two threads per key, rows 0-31 and 32-63, then the pair
+    const int kk = tid >> 1, half = tid & 1;
+    float acc = 0.0f;
+    for (int rr = 32 * half; rr < 32 * half + 32; ++rr) acc += ahat[kk * APITCH + rr];
+    const float other = __shfl_xor(acc, 1);
+    const float tot = half == 0 ? acc + other : other + acc;
+    const int kap = t * B + kk;
+    if (half == 0 && kap < jb.L_c) jb.v[kap] = tot;
+  }
+  if (jb.dpart) {   // diagonal d = r - kk + 63, d in [0, 127)
+    const int d = tid;
+    float acc = 0.0f;
+    if (d < 127) {
+      const int rlo = max(0, d - 63), rhi = min(63, d);
+      for (int rr = rlo; rr <= rhi; ++rr) acc += ahat[(rr + 63 - d) * APITCH + rr];
+    }
+    jb.dpart[(int64_t)t * 128 + d] = acc;
+  }
+}
+
+__device__ __forceinline__ int floordiv(int a, int b) {
+  int q = a / b;
+  return (a % b != 0 && ((a < 0) != (b < 0))) ? q - 1 : q;
+}
+
+// u[o] = sum over tiles t (ascending) of dpart[t][o - coord0 + 64 t + 63].
+__global__ __launch_bounds__(256) void k_est_udiag(const EstJob* jobs) {
+  const EstJob jb = jobs[blockIdx.x];
+  if (!jb.u) return;
+  const int o = blockIdx.y * 256 + threadIdx.x;
+  if (o >= jb.L_c) return;
+  const int base = jb.coord0 - o;
+  const int tlo = max(0, -floordiv(-(base - 63), 64));   // ceil((base - 63) / 64)
+  const int thi = min(jb.ntiles - 1, floordiv(base + 63, 64));
+  float acc = 0.0f;
+  for (int t = tlo; t <= thi; ++t) {
+    const int d = o - jb.coord0 + 64 * t + 63;
+    if (d >= 0 && d < 127) acc += jb.dpart[(int64_t)t * 128 + d];
+  }
+  jb.u[o] = acc;
+}
+
+hipError_t launch_est_lse(const RowSet* rs, int nrs, int max_chunks, Tensor q, Tensor k, int chunk_keys,
+                          hipStream_t st) {
+  if (nrs <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_est_lse, dim3(nrs, max_chunks), dim3(128), 0, st, rs, q, k, chunk_keys);
+  hipLaunchKernelGGL(k_est_merge, dim3(nrs), dim3(64), 0, st, rs);
+  return hipGetLastError();
+}
+
+hipError_t launch_est_scores(const EstJob* jobs, int njobs, int max_tiles, const RowSet* rs, Tensor q,
+                             Tensor k, hipStream_t st) {
+  if (njobs <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_est_scores, dim3(njobs, max_tiles), dim3(128), 0, st, jobs, rs, q, k);
+  return hipGetLastError();
+}
+
+hipError_t launch_est_udiag(const EstJob* jobs, int njobs, int max_L, hipStream_t st) {
+  if (njobs <= 0 || max_L <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_est_udiag, dim3(njobs, (max_L + 255) / 256), dim3(256), 0, st, jobs);
+  return hipGetLastError();
+}
+
+}  // namespace mmi

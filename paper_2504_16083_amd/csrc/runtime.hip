@@ -1,0 +1,957 @@
+// Host runtime of libmmi: argument validation, modality layout, the plan
+// (estimation jobs, choices, permutations, block index, work list), launch
+// sequencing on the caller's stream, a caching device allocator, and the
+// C entry points declared in include/mmi.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <stdexcept>
+#include <string>
+#include <vector>
+
+#include "device.hpp"
+#include "internal.hpp"
+
+namespace mmi {
+
+// ------------------------------------------------------------------ errors
+struct Error : std::runtime_error {
+  int code;
+  Error(int c, const std::string& m) : std::runtime_error(m), code(c) {}
+};
+
+static thread_local std::string g_last_error;
+
+[[noreturn]] static void fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  throw Error(code, buf);
+}
+
+#define HIPCHK(expr)                                                                          \
+  do {                                                                                        \
+    hipError_t e_ = (expr);                                                                   \
+    if (e_ != hipSuccess) fail(MMI_ERR_HIP, "%s: %s (%s:%d)", #expr, hipGetErrorString(e_), \
+                               __FILE__, __LINE__);                                           \
+  } while (0)
+
+// ------------------------------------------------------------------ allocator
+// Device memory cache owned by a context: freed blocks are kept per exact
+// size and handed out again, so repeated plans of one shape allocate once.
+class Allocator {
+ public:
+  ~Allocator() { release(); }
+  void* get(size_t bytes) {
+    bytes = round(bytes);
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      auto it = free_.find(bytes);
+      if (it != free_.end()) {
+        void* p = it->second;
+        free_.erase(it);
+        return p;
+      }
+    }
+    void* p = nullptr;
+    if (hipMalloc(&p, bytes) != hipSuccess) {
+      (void)hipGetLastError();
+      release();
+      if (hipMalloc(&p, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        fail(MMI_ERR_OOM, "device allocation of %zu bytes failed", bytes);
+      }
+    }
+    return p;
+  }
+  void put(void* p, size_t bytes) {
+    if (!p) return;
+    std::lock_guard<std::mutex> lk(mu_);
+    free_.emplace(round(bytes), p);
+  }
+  void release() {
+    std::lock_guard<std::mutex> lk(mu_);
+    for (auto& kv : free_) (void)hipFree(kv.second);
+    free_.clear();
+  }
+
+ private:
+  static size_t round(size_t b) {
+    if (b < 256) return 256;
+    size_t r = 256;
+    while (r < b && r < ((size_t)1 << 24)) r <<= 1;
+    if (r >= b) return r;
+    return (b + ((size_t)1 << 24) - 1) & ~(((size_t)1 << 24) - 1);
+  }
+  std::mutex mu_;
+  std::multimap<size_t, void*> free_;
+};
+
+}  // namespace mmi
+
+struct mmi_ctx {
+  int device = 0;
+  int chunk_blocks = 128;
+  mmi::Allocator alloc;
+  int64_t* pinned = nullptr;       // host staging for totals
+  size_t pinned_n = 0;
+};
+
+namespace mmi {
+
+// ------------------------------------------------------------------ plan
+struct Buf {
+  void* p = nullptr;
+  size_t n = 0;
+};
+
+struct EstInfo {       // host view of one estimation job
+  int job = -1;
+  int rowset = -1;
+  int L_c = 0, nrows = 0, row0 = 0;
+  float* v = nullptr;
+  float* u = nullptr;
+  float* fold = nullptr;
+  int lo = 0, hi = -1;
+  int32_t* params = nullptr;
+  int32_t* vsel = nullptr;
+  int32_t* ssel = nullptr;
+  int nv = 0, ns = 0;
+};
+
+struct HostHead {
+  int kind = 0;
+  int op0 = 0, nops = 0;
+  std::vector<int> op_slot;      // op index -> export slot
+  std::vector<EstInfo> est;      // per op
+  int64_t nnz = 0, nitems = 0, nsplit = 0, nparts = 0;
+};
+
+}  // namespace mmi
+
+struct mmi_plan {
+  mmi_ctx* ctx = nullptr;
+  hipStream_t stream = nullptr;
+  mmi_problem prob{};
+  int S = 0, Hq = 0, Hkv = 0;
+  mmi::Groups groups{};
+  std::vector<mmi::Buf> bufs;
+  std::vector<mmi::HeadDev> heads;
+  std::vector<mmi::OpDev> ops;
+  std::vector<mmi::HostHead> hh;
+  mmi::HeadDev* d_heads = nullptr;
+  mmi::OpDev* d_ops = nullptr;
+  mmi::WorkItem* d_items = nullptr;
+  mmi::SplitRow* d_splits = nullptr;
+  float* d_part_o = nullptr;
+  float* d_part_ml = nullptr;
+  int64_t nitems = 0, nsplit = 0, nparts = 0;
+  int32_t* d_tpos = nullptr;
+  std::vector<float*> est_lse2;  // per rowset
+  std::vector<std::vector<uint8_t>> keep;   // host sources of asynchronous uploads
+  std::vector<int> rowset_n;
+};
+
+namespace mmi {
+
+template <typename T>
+static T* dalloc(mmi_plan* P, size_t count) {
+  size_t bytes = std::max<size_t>(count, 1) * sizeof(T);
+  void* p = P->ctx->alloc.get(bytes);
+  P->bufs.push_back({p, bytes});
+  return reinterpret_cast<T*>(p);
+}
+
+// The host copy is kept in the plan until it is destroyed, so the
+// asynchronous copy never reads freed memory.
+template <typename T>
+static T* upload(mmi_plan* P, const std::vector<T>& v) {
+  T* d = dalloc<T>(P, v.size());
+  if (!v.empty()) {
+    P->keep.emplace_back(reinterpret_cast<const uint8_t*>(v.data()),
+                         reinterpret_cast<const uint8_t*>(v.data()) + v.size() * sizeof(T));
+    HIPCHK(hipMemcpyAsync(d, P->keep.back().data(), v.size() * sizeof(T), hipMemcpyHostToDevice, P->stream));
+  }
+  return d;
+}
+
+static void free_plan_buffers(mmi_plan* P) {
+  for (auto& b : P->bufs) P->ctx->alloc.put(b.p, b.n);
+  P->bufs.clear();
+}
+
+// ------------------------------------------------------------------ validation
+static void check_op(const mmi_op& op, std::initializer_list<int> allowed, const char* where, int h) {
+  bool ok = false;
+  for (int a : allowed) ok |= (op.kind == a);
+  if (!ok) fail(MMI_ERR_BAD_CONFIG, "head %d: op kind %d not allowed for %s", h, op.kind, where);
+  if (op.kind == MMI_OP_ASHAPE && (op.sink < 0 || op.local < 0))
+    fail(MMI_ERR_BAD_CONFIG, "head %d: A-shape sink/local must be >= 0", h);
+  if ((op.kind == MMI_OP_VSLASH || op.kind == MMI_OP_VERT) && (op.n_vertical < 0 || op.n_slash < 0))
+    fail(MMI_ERR_BAD_CONFIG, "head %d: vertical/slash sizes must be >= 0", h);
+  if (op.kind == MMI_OP_GRID &&
+      (op.stride_lo < 1 || op.stride_hi < op.stride_lo || op.stride_hi > MMI_MAX_STRIDE))
+    fail(MMI_ERR_BAD_CONFIG, "head %d: grid stride range [%d, %d] outside [1, %d]", h, op.stride_lo,
+         op.stride_hi, MMI_MAX_STRIDE);
+}
+
+static void aligned16(const void* p, const char* name) {
+  if (reinterpret_cast<uintptr_t>(p) % 16) fail(MMI_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+}
+
+static mmi_problem normalise(const mmi_problem* pr) {
+  if (!pr) fail(MMI_ERR_INVALID_ARG, "problem is NULL");
+  mmi_problem p = *pr;
+  if (p.S < 1) fail(MMI_ERR_INVALID_ARG, "S must be >= 1");
+  if (p.S > MMI_MAX_SEQ) fail(MMI_ERR_UNSUPPORTED, "S = %lld exceeds %d", (long long)p.S, MMI_MAX_SEQ);
+  if (p.Hq < 1 || p.Hkv < 1) fail(MMI_ERR_INVALID_ARG, "head counts must be >= 1");
+  if (p.Hq % p.Hkv) fail(MMI_ERR_UNSUPPORTED, "Hq %% Hkv != 0");
+  if (p.D != MMI_HEAD_DIM) fail(MMI_ERR_UNSUPPORTED, "head dim %d (only 128)", p.D);
+  if (p.block != MMI_BLOCK) fail(MMI_ERR_UNSUPPORTED, "block %d (only 64)", p.block);
+  auto def = [](int64_t& ss, int64_t& sh, int H) {
+    if (ss == 0 && sh == 0) { ss = (int64_t)H * 128; sh = 128; }
+  };
+  def(p.q_stride_s, p.q_stride_h, p.Hq);
+  def(p.k_stride_s, p.k_stride_h, p.Hkv);
+  def(p.v_stride_s, p.v_stride_h, p.Hkv);
+  def(p.o_stride_s, p.o_stride_h, p.Hq);
+  const int64_t st[8] = {p.q_stride_s, p.q_stride_h, p.k_stride_s, p.k_stride_h,
+                         p.v_stride_s, p.v_stride_h, p.o_stride_s, p.o_stride_h};
+  for (int i = 0; i < 8; ++i)
+    if (st[i] <= 0 || st[i] % 8) fail(MMI_ERR_INVALID_ARG, "strides must be positive multiples of 8 elements");
+  if (p.modality) {
+    if (p.n_modalities < 1 || p.n_modalities > MMI_MAX_MODALITIES)
+      fail(MMI_ERR_INVALID_ARG, "n_modalities must be in [1, %d]", MMI_MAX_MODALITIES);
+    for (int64_t i = 0; i < p.S; ++i)
+      if (p.modality[i] >= p.n_modalities) fail(MMI_ERR_INVALID_ARG, "modality[%lld] = %d out of range",
+                                                (long long)i, (int)p.modality[i]);
+  }
+  return p;
+}
+
+// ------------------------------------------------------------------ layout (host)
+struct Layout {
+  std::vector<Segment> segs;
+  Groups g{};
+  int gidx_of_mod[MMI_MAX_MODALITIES];
+  std::vector<std::vector<int>> seg_of_group;   // segment indices per group, ascending
+};
+
+static Layout make_layout(const mmi_problem& p) {
+  Layout L;
+  const int S = (int)p.S;
+  int count[MMI_MAX_MODALITIES] = {0};
+  if (!p.modality) {
+    L.segs.push_back({0, S, 0, 0});
+    count[0] = S;
+  } else {
+    int i = 0;
+    while (i < S) {
+      int j = i;
+      const int m = p.modality[i];
+      while (j < S && p.modality[j] == m) ++j;
+      L.segs.push_back({i, j - i, count[m], m});
+      count[m] += j - i;
+      i = j;
+    }
+  }
+  std::fill(L.gidx_of_mod, L.gidx_of_mod + MMI_MAX_MODALITIES, -1);
+  int off = 0, toff = 0;
+  for (int m = 0; m < MMI_MAX_MODALITIES; ++m) {
+    if (!count[m]) continue;
+    const int gi = L.g.n++;
+    L.gidx_of_mod[m] = gi;
+    L.g.mod[gi] = m;
+    L.g.off[gi] = off;
+    L.g.len[gi] = count[m];
+    L.g.toff[gi] = toff;
+    off += (count[m] + B - 1) / B * B;
+    toff += count[m];
+  }
+  L.seg_of_group.resize(L.g.n);
+  for (int s = 0; s < (int)L.segs.size(); ++s) L.seg_of_group[L.gidx_of_mod[L.segs[s].mod]].push_back(s);
+  return L;
+}
+
+// final <= 64 positions of the last run of group gi -> (row0, nrows, local index of row0)
+static void final_rows(const Layout& L, int gi, int& row0, int& nrows, int& loc0) {
+  const Segment& s = L.segs[L.seg_of_group[gi].back()];
+  nrows = std::min(LASTQ, s.len);
+  row0 = s.pos + s.len - nrows;
+  loc0 = s.loc + s.len - nrows;
+}
+
+// number of positions of group gi that are <= pos
+static int count_le(const Layout& L, int gi, int pos) {
+  int c = 0;
+  for (int s : L.seg_of_group[gi]) {
+    const Segment& sg = L.segs[s];
+    if (sg.pos > pos) break;
+    c += std::min(sg.len, pos - sg.pos + 1);
+  }
+  return c;
+}
+
+// ------------------------------------------------------------------ plan create
+struct Builder {
+  mmi_plan* P;
+  Layout L;
+  std::vector<RowSet> rowsets;
+  std::vector<EstJob> jobs;
+  std::vector<GridJob> gjobs;
+  std::vector<TopkJob> tjobs;
+  std::map<std::pair<int, int>, int> rowset_of;   // (head, row0) -> index
+  int chunk_keys = 4096;
+  int max_tiles = 0, max_L = 0, max_chunks = 0, max_cands = 0, max_sel = 0;
+  int32_t* d_tpos = nullptr;
+
+  int rowset(int head, int kvh, int row0, int nrows) {
+    auto key = std::make_pair(head, row0);
+    auto it = rowset_of.find(key);
+    if (it != rowset_of.end()) return it->second;
+    RowSet r{};
+    r.head = head; r.kvh = kvh; r.row0 = row0; r.nrows = nrows;
+    r.nchunks = (row0 + nrows + chunk_keys - 1) / chunk_keys;
+    r.part = dalloc<float>(P, (size_t)r.nchunks * LASTQ * 2);
+    r.lse2 = dalloc<float>(P, LASTQ);
+    max_chunks = std::max(max_chunks, r.nchunks);
+    rowsets.push_back(r);
+    P->est_lse2.push_back(r.lse2);
+    P->rowset_n.push_back(nrows);
+    return rowset_of[key] = (int)rowsets.size() - 1;
+  }
+
+  // estimation job; gi_key = key group (-1 = global positions)
+  EstInfo est(int head, int kvh, int row0, int nrows, int coord0, int gi_key, int L_c, bool need_u) {
+    EstInfo e;
+    e.rowset = rowset(head, kvh, row0, nrows);
+    EstJob j{};
+    j.head = head; j.kvh = kvh; j.row0 = row0; j.nrows = nrows; j.rowset = e.rowset;
+    j.coord0 = coord0;
+    j.keymap = gi_key >= 0 ? d_tpos + L.g.toff[gi_key] : nullptr;
+    j.L_c = L_c;
+    j.ntiles = (L_c + B - 1) / B;
+    j.v = dalloc<float>(P, L_c);
+    j.u = need_u ? dalloc<float>(P, L_c) : nullptr;
+    j.dpart = need_u ? dalloc<float>(P, (size_t)j.ntiles * 128) : nullptr;
+    max_tiles = std::max(max_tiles, j.ntiles);
+    max_L = std::max(max_L, L_c);
+    e.job = (int)jobs.size();
+    e.L_c = L_c; e.nrows = nrows; e.row0 = row0;
+    e.v = j.v; e.u = j.u;
+    jobs.push_back(j);
+    return e;
+  }
+
+  void grid(EstInfo& e, const mmi_op& op, int32_t* params) {
+    GridJob gj{};
+    gj.v = e.v;
+    gj.L_c = e.L_c;
+    gj.lo = std::max(1, op.stride_lo);
+    gj.hi = std::min(op.stride_hi, e.L_c / 2);
+    const int nc = std::max(0, gj.hi - gj.lo + 1);
+    gj.fold = dalloc<float>(P, (size_t)std::max(nc, 1) * FOLD_W);
+    gj.score = dalloc<float>(P, std::max(nc, 1));
+    gj.pick = dalloc<int32_t>(P, std::max(nc, 1));
+    gj.params = params;
+    gj.nrows = e.nrows;
+    max_cands = std::max(max_cands, nc);
+    e.fold = gj.fold; e.lo = gj.lo; e.hi = gj.hi; e.params = params;
+    gjobs.push_back(gj);
+  }
+
+  int32_t* topk(const float* x, int L, int n) {
+    n = std::min(n, L);
+    int32_t* out = dalloc<int32_t>(P, std::max(n, 1));
+    if (n > 0) tjobs.push_back({x, L, n, out});
+    max_sel = std::max(max_sel, n);
+    return out;
+  }
+};
+
+static void validate_cfgs(const Groups& g, const mmi_problem& p, const mmi_head_cfg* cfgs) {
+  for (int h = 0; h < p.Hq; ++h) {
+    const mmi_head_cfg& c = cfgs[h];
+    if (c.kind == MMI_HEAD_GLOBAL) {
+      check_op(c.global, {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH, MMI_OP_GRID}, "a global head", h);
+    } else if (c.kind == MMI_HEAD_QBOUNDARY) {
+      for (int gi = 0; gi < g.n; ++gi)
+        check_op(c.intra[g.mod[gi]], {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH}, "a Q-Boundary modality", h);
+    } else if (c.kind == MMI_HEAD_2D) {
+      for (int a = 0; a < g.n; ++a)
+        for (int b2 = 0; b2 < g.n; ++b2) {
+          if (a == b2)
+            check_op(c.intra[g.mod[a]], {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH, MMI_OP_GRID},
+                     "a 2D-Boundary intra pair", h);
+          else
+            check_op(c.cross[g.mod[a]][g.mod[b2]], {MMI_OP_NONE, MMI_OP_DENSE, MMI_OP_VERT},
+                     "a 2D-Boundary cross pair", h);
+        }
+    } else {
+      fail(MMI_ERR_BAD_CONFIG, "head %d: unknown head kind %d", h, c.kind);
+    }
+  }
+
+}
+
+static void validate_inputs(const mmi_problem* prob, const mmi_head_cfg* cfgs, const void* q, const void* k) {
+  const mmi_problem p = normalise(prob);
+  if (!cfgs) fail(MMI_ERR_INVALID_ARG, "cfgs is NULL");
+  if (!q || !k) fail(MMI_ERR_INVALID_ARG, "q/k is NULL");
+  aligned16(q, "q");
+  aligned16(k, "k");
+  const Layout L = make_layout(p);
+  validate_cfgs(L.g, p, cfgs);
+}
+
+static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi_head_cfg* cfgs, const void* q,
+                             const void* k, hipStream_t st, mmi_plan* P) {
+  const mmi_problem p = normalise(prob_in);
+  if (!cfgs) fail(MMI_ERR_INVALID_ARG, "cfgs is NULL");
+  if (!q || !k) fail(MMI_ERR_INVALID_ARG, "q/k is NULL");
+  aligned16(q, "q");
+  aligned16(k, "k");
+  P->ctx = ctx;
+  P->stream = st;
+  P->prob = p;
+  P->prob.modality = nullptr;
+  P->S = (int)p.S; P->Hq = p.Hq; P->Hkv = p.Hkv;
+  const int S = P->S, G = p.Hq / p.Hkv;
+  Builder bd{P};
+  bd.L = make_layout(p);
+  const Layout& L = bd.L;
+  const Groups& g = L.g;
+  P->groups = g;
+  validate_cfgs(g, p, cfgs);
+
+  HIPCHK(hipSetDevice(ctx->device));
+  // positions of each modality
+  std::vector<int32_t> toff_by_mod(MMI_MAX_MODALITIES, 0);
+  for (int gi = 0; gi < g.n; ++gi) toff_by_mod[g.mod[gi]] = g.toff[gi];
+  Segment* d_segs = upload(P, L.segs);
+  int32_t* d_toff = upload(P, toff_by_mod);
+  bd.d_tpos = P->d_tpos = dalloc<int32_t>(P, S);
+  HIPCHK(launch_positions(d_segs, (int)L.segs.size(), d_toff, bd.d_tpos, S, st));
+
+  const int nb_all = (S + B - 1) / B;
+  int nb_groups = 0;
+  for (int gi = 0; gi < g.n; ++gi) nb_groups += (g.len[gi] + B - 1) / B;
+
+  P->hh.resize(p.Hq);
+  int max_slots = 0, max_nbq = 0, max_nbk = 0;
+  for (int h = 0; h < p.Hq; ++h) {
+    const mmi_head_cfg& c = cfgs[h];
+    HostHead& H = P->hh[h];
+    HeadDev hd{};
+    hd.kind = c.kind;
+    hd.kvh = h / G;
+    hd.S = S;
+    hd.op0 = (int)P->ops.size();
+    H.kind = c.kind;
+    H.op0 = hd.op0;
+    auto base_op = [&](const mmi_op& o) {
+      OpDev d{};
+      d.kind = o.kind;
+      d.sink = o.sink; d.local = o.local;
+      d.use_h = o.use_h != 0; d.use_v = o.use_v != 0; d.use_s = o.use_s != 0;
+      return d;
+    };
+    if (c.kind == MMI_HEAD_GLOBAL) {
+      hd.nbq = hd.nbk = nb_all;
+      OpDev d = base_op(c.global);
+      d.L = S; d.kbase = 0; d.nkblk = nb_all;
+      EstInfo e;
+      const int nrows = std::min(LASTQ, S), row0 = S - nrows;
+      if (c.global.kind == MMI_OP_GRID || c.global.kind == MMI_OP_VSLASH) {
+        e = bd.est(h, hd.kvh, row0, nrows, row0, -1, S, c.global.kind == MMI_OP_VSLASH);
+        if (c.global.kind == MMI_OP_GRID) {
+          int32_t* params = dalloc<int32_t>(P, 4);
+          bd.grid(e, c.global, params);
+          d.params = params;
+        } else {
+          e.vsel = bd.topk(e.v, e.L_c, c.global.n_vertical);
+          e.ssel = bd.topk(e.u, e.L_c, c.global.n_slash);
+          e.nv = std::min(c.global.n_vertical, e.L_c);
+          e.ns = std::min(c.global.n_slash, e.L_c);
+          d.vsel = e.vsel; d.nv = e.nv; d.ssel = e.ssel; d.ns = e.ns;
+          d.minsel = dalloc<int32_t>(P, nb_all);
+        }
+      }
+      if (c.global.kind == MMI_OP_GRID) {
+        hd.qperm = dalloc<int32_t>(P, (size_t)nb_all * B);
+        hd.kperm = hd.qperm;
+        hd.kminpos = dalloc<int32_t>(P, nb_all);
+      }
+      P->ops.push_back(d);
+      H.est.push_back(e);
+      H.op_slot.push_back(0);
+    } else if (c.kind == MMI_HEAD_QBOUNDARY) {
+      hd.nbq = nb_groups;
+      hd.nbk = nb_all;
+      hd.qperm = dalloc<int32_t>(P, (size_t)nb_groups * B);
+      for (int gi = 0; gi < g.n; ++gi) {
+        const mmi_op& o = c.intra[g.mod[gi]];
+        OpDev d = base_op(o);
+        d.L = S; d.kbase = 0; d.nkblk = nb_all;
+        EstInfo e;
+        if (o.kind == MMI_OP_VSLASH) {
+          int row0, nrows, loc0;
+          final_rows(L, gi, row0, nrows, loc0);
+          e = bd.est(h, hd.kvh, row0, nrows, row0, -1, row0 + nrows, true);
+          e.vsel = bd.topk(e.v, e.L_c, o.n_vertical);
+          e.ssel = bd.topk(e.u, e.L_c, o.n_slash);
+          e.nv = std::min(o.n_vertical, e.L_c);
+          e.ns = std::min(o.n_slash, e.L_c);
+          d.vsel = e.vsel; d.nv = e.nv; d.ssel = e.ssel; d.ns = e.ns;
+          d.minsel = dalloc<int32_t>(P, nb_all);
+        }
+        P->ops.push_back(d);
+        H.est.push_back(e);
+        H.op_slot.push_back(g.mod[gi]);
+      }
+    } else {
+      hd.nbq = hd.nbk = nb_groups;
+      hd.qperm = dalloc<int32_t>(P, (size_t)nb_groups * B);
+      hd.kperm = hd.qperm;
+      hd.kminpos = dalloc<int32_t>(P, nb_groups);
+      const int n0 = (int)P->ops.size();
+      P->ops.resize(n0 + g.n * g.n);
+      H.est.resize(g.n * g.n);
+      H.op_slot.resize(g.n * g.n);
+      // intra ops first (cross VERT into a Grid group needs that group's params)
+      for (int gi = 0; gi < g.n; ++gi) {
+        const mmi_op& o = c.intra[g.mod[gi]];
+        OpDev d = base_op(o);
+        d.L = g.len[gi]; d.kbase = g.off[gi] / B; d.nkblk = (g.len[gi] + B - 1) / B;
+        d.keymap = bd.d_tpos + g.toff[gi];
+        d.koff = g.off[gi];
+        EstInfo e;
+        if (o.kind == MMI_OP_GRID || o.kind == MMI_OP_VSLASH) {
+          int row0, nrows, loc0;
+          final_rows(L, gi, row0, nrows, loc0);
+          e = bd.est(h, hd.kvh, row0, nrows, loc0, gi, g.len[gi], o.kind == MMI_OP_VSLASH);
+          if (o.kind == MMI_OP_GRID) {
+            int32_t* params = dalloc<int32_t>(P, 4);
+            bd.grid(e, o, params);
+            d.params = params;
+          } else {
+            e.vsel = bd.topk(e.v, e.L_c, o.n_vertical);
+            e.ssel = bd.topk(e.u, e.L_c, o.n_slash);
+            e.nv = std::min(o.n_vertical, e.L_c);
+            e.ns = std::min(o.n_slash, e.L_c);
+            d.vsel = e.vsel; d.nv = e.nv; d.ssel = e.ssel; d.ns = e.ns;
+            d.minsel = dalloc<int32_t>(P, d.nkblk);
+          }
+        }
+        P->ops[n0 + gi * g.n + gi] = d;
+        H.est[gi * g.n + gi] = e;
+        H.op_slot[gi * g.n + gi] = g.mod[gi];
+      }
+      for (int a = 0; a < g.n; ++a)
+        for (int b2 = 0; b2 < g.n; ++b2) {
+          if (a == b2) continue;
+          const mmi_op& o = c.cross[g.mod[a]][g.mod[b2]];
+          OpDev d = base_op(o);
+          d.L = g.len[b2]; d.kbase = g.off[b2] / B; d.nkblk = (g.len[b2] + B - 1) / B;
+          d.keymap = bd.d_tpos + g.toff[b2];
+          d.koff = g.off[b2];
+          const OpDev& kintra = P->ops[n0 + b2 * g.n + b2];
+          d.kgrid = kintra.kind == MMI_OP_GRID ? 1 : 0;
+          d.kparams = kintra.params;
+          EstInfo e;
+          if (o.kind == MMI_OP_VERT) {
+            int row0, nrows, loc0;
+            final_rows(L, a, row0, nrows, loc0);
+            const int Lc = count_le(L, b2, row0 + nrows - 1);
+            if (Lc > 0) {
+              e = bd.est(h, hd.kvh, row0, nrows, 0, b2, Lc, false);
+              e.vsel = bd.topk(e.v, e.L_c, o.n_vertical);
+              e.nv = std::min(o.n_vertical, e.L_c);
+            }
+            d.vsel = e.vsel; d.nv = e.nv;
+            d.minsel = dalloc<int32_t>(P, d.nkblk);
+          }
+          P->ops[n0 + a * g.n + b2] = d;
+          H.est[a * g.n + b2] = e;
+          H.op_slot[a * g.n + b2] = 8 + g.mod[a] * 8 + g.mod[b2];
+        }
+    }
+    H.nops = (int)P->ops.size() - H.op0;
+    hd.nwords = (hd.nbk + 31) / 32;
+    hd.counts = dalloc<int32_t>(P, hd.nbq);
+    hd.chunks = dalloc<int32_t>(P, hd.nbq);
+    hd.itembase = dalloc<int32_t>(P, hd.nbq);
+    hd.splitoff = dalloc<int32_t>(P, hd.nbq);
+    hd.partoff = dalloc<int32_t>(P, hd.nbq);
+    hd.rowptr = dalloc<int32_t>(P, hd.nbq + 1);
+    hd.bitmap = dalloc<uint32_t>(P, (size_t)hd.nbq * hd.nwords);
+    max_slots = std::max(max_slots, hd.nbq * B);
+    max_nbq = std::max(max_nbq, hd.nbq);
+    max_nbk = std::max(max_nbk, hd.nbk);
+    P->heads.push_back(hd);
+  }
+
+  // estimation -> choices
+  const Tensor tq{q, p.q_stride_s, p.q_stride_h}, tk{k, p.k_stride_s, p.k_stride_h};
+  RowSet* d_rs = upload(P, bd.rowsets);
+  EstJob* d_jobs = upload(P, bd.jobs);
+  HIPCHK(launch_est_lse(d_rs, (int)bd.rowsets.size(), bd.max_chunks, tq, tk, bd.chunk_keys, st));
+  HIPCHK(launch_est_scores(d_jobs, (int)bd.jobs.size(), bd.max_tiles, d_rs, tq, tk, st));
+  HIPCHK(launch_est_udiag(d_jobs, (int)bd.jobs.size(), bd.max_L, st));
+  GridJob* d_g = upload(P, bd.gjobs);
+  HIPCHK(launch_grid_search(d_g, (int)bd.gjobs.size(), bd.max_cands, st));
+  TopkJob* d_t = upload(P, bd.tjobs);
+  HIPCHK(launch_topk(d_t, (int)bd.tjobs.size(), st));
+
+  // permutations, key summaries, block counts
+  P->d_heads = upload(P, P->heads);
+  P->d_ops = upload(P, P->ops);
+  HIPCHK(launch_perms(P->d_heads, p.Hq, P->d_ops, g, bd.d_tpos, S, max_slots, st));
+  HIPCHK(launch_key_summaries(P->d_heads, p.Hq, P->d_ops, (int)P->ops.size(), g, max_nbk, bd.max_sel, st));
+  const int chunk = ctx->chunk_blocks;
+  HIPCHK(launch_blocks_count(P->d_heads, p.Hq, P->d_ops, g, bd.d_tpos, d_segs, (int)L.segs.size(), max_nbq,
+                             chunk, st));
+  int64_t* d_tot = dalloc<int64_t>(P, (size_t)p.Hq * 4);
+  HIPCHK(launch_blocks_scan(P->d_heads, p.Hq, d_tot, st));
+  if (ctx->pinned_n < (size_t)p.Hq * 4) {
+    if (ctx->pinned) HIPCHK(hipHostFree(ctx->pinned));
+    ctx->pinned = nullptr;
+    HIPCHK(hipHostMalloc((void**)&ctx->pinned, sizeof(int64_t) * p.Hq * 4));
+    ctx->pinned_n = (size_t)p.Hq * 4;
+  }
+  HIPCHK(hipMemcpyAsync(ctx->pinned, d_tot, sizeof(int64_t) * p.Hq * 4, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipStreamSynchronize(st));
+
+  // sizes known: column pool, work items, partials
+  std::vector<int64_t> item_base(p.Hq), part_base(p.Hq), split_base(p.Hq);
+  int64_t nnz_all = 0;
+  for (int h = 0; h < p.Hq; ++h) {
+    HostHead& H = P->hh[h];
+    H.nnz = ctx->pinned[h * 4 + 0];
+    H.nitems = ctx->pinned[h * 4 + 1];
+    H.nsplit = ctx->pinned[h * 4 + 2];
+    H.nparts = ctx->pinned[h * 4 + 3];
+    item_base[h] = P->nitems;
+    part_base[h] = P->nparts;
+    split_base[h] = P->nsplit;
+    P->nitems += H.nitems;
+    P->nparts += H.nparts;
+    P->nsplit += H.nsplit;
+    nnz_all += H.nnz;
+  }
+  if (P->nitems > 0x7fffffff || P->nparts > 0x7fffffff)
+    fail(MMI_ERR_UNSUPPORTED, "work list too large (%lld items)", (long long)P->nitems);
+  int32_t* col = dalloc<int32_t>(P, nnz_all);
+  int64_t off = 0;
+  for (int h = 0; h < p.Hq; ++h) {
+    P->heads[h].col = col + off;
+    off += P->hh[h].nnz;
+  }
+  P->keep.emplace_back(reinterpret_cast<const uint8_t*>(P->heads.data()),
+                       reinterpret_cast<const uint8_t*>(P->heads.data()) + sizeof(HeadDev) * p.Hq);
+  HIPCHK(hipMemcpyAsync(P->d_heads, P->keep.back().data(), sizeof(HeadDev) * p.Hq, hipMemcpyHostToDevice, st));
+  HIPCHK(launch_blocks_fill(P->d_heads, p.Hq, max_nbq, st));
+  P->d_items = dalloc<WorkItem>(P, P->nitems);
+  P->d_splits = dalloc<SplitRow>(P, P->nsplit);
+  P->d_part_o = dalloc<float>(P, (size_t)std::max<int64_t>(P->nparts, 1) * B * D);
+  P->d_part_ml = dalloc<float>(P, (size_t)std::max<int64_t>(P->nparts, 1) * B * 2);
+  int64_t* d_ib = upload(P, item_base);
+  int64_t* d_pb = upload(P, part_base);
+  int64_t* d_sb = upload(P, split_base);
+  HIPCHK(launch_work_fill(P->d_heads, p.Hq, d_ib, d_pb, d_sb, max_nbq, chunk, P->d_items, P->d_splits, st));
+}
+
+static void plan_execute_impl(mmi_plan* P, const void* q, const void* k, const void* v, void* o, float* lse,
+                              hipStream_t st) {
+  if (!q || !k || !v || !o) fail(MMI_ERR_INVALID_ARG, "q/k/v/o is NULL");
+  aligned16(q, "q"); aligned16(k, "k"); aligned16(v, "v"); aligned16(o, "o");
+  if (o == q || o == k || o == v) fail(MMI_ERR_INVALID_ARG, "o aliases an input");
+  HIPCHK(hipSetDevice(P->ctx->device));
+  const mmi_problem& p = P->prob;
+  AttnArgs a{};
+  a.q = {q, p.q_stride_s, p.q_stride_h};
+  a.k = {k, p.k_stride_s, p.k_stride_h};
+  a.v = {v, p.v_stride_s, p.v_stride_h};
+  a.o = o; a.o_ss = p.o_stride_s; a.o_sh = p.o_stride_h;
+  a.lse = lse;
+  a.S = P->S;
+  a.heads = P->d_heads;
+  a.items = P->d_items;
+  a.nitems = P->nitems;
+  a.part_o = P->d_part_o;
+  a.part_ml = P->d_part_ml;
+  HIPCHK(launch_attention(a, st));
+  HIPCHK(launch_combine(a, P->d_splits, P->nsplit, st));
+  P->stream = st;
+}
+
+}  // namespace mmi
+
+// ====================================================================== C ABI
+using namespace mmi;
+
+template <typename F>
+static int guarded(F&& f) {
+  try {
+    f();
+    return MMI_OK;
+  } catch (const Error& e) {
+    g_last_error = e.what();
+    return e.code;
+  } catch (const std::bad_alloc&) {
+    g_last_error = "host allocation failed";
+    return MMI_ERR_OOM;
+  } catch (const std::exception& e) {
+    g_last_error = e.what();
+    return MMI_ERR_INTERNAL;
+  } catch (...) {
+    g_last_error = "unknown error";
+    return MMI_ERR_INTERNAL;
+  }
+}
+
+extern "C" {
+
+int mmi_version(void) { return MMI_ABI_VERSION; }
+
+const char* mmi_status_str(int s) {
+  switch (s) {
+    case MMI_OK: return "ok";
+    case MMI_ERR_INVALID_ARG: return "invalid argument";
+    case MMI_ERR_UNSUPPORTED: return "unsupported shape";
+    case MMI_ERR_BAD_CONFIG: return "bad head config";
+    case MMI_ERR_OOM: return "out of device memory";
+    case MMI_ERR_HIP: return "HIP runtime error";
+    case MMI_ERR_STATE: return "invalid state";
+    case MMI_ERR_INTERNAL: return "internal error";
+    default: return "unknown status";
+  }
+}
+
+const char* mmi_last_error(void) { return g_last_error.c_str(); }
+
+int mmi_ctx_create(int device, mmi_ctx** out) {
+  return guarded([&] {
+    if (!out) fail(MMI_ERR_INVALID_ARG, "out is NULL");
+    int n = 0;
+    HIPCHK(hipGetDeviceCount(&n));
+    if (device < 0 || device >= n) fail(MMI_ERR_INVALID_ARG, "device %d of %d", device, n);
+    HIPCHK(hipSetDevice(device));
+    auto* c = new mmi_ctx();
+    c->device = device;
+    if (const char* e = getenv("MMI_CHUNK_BLOCKS")) {
+      const int v = atoi(e);
+      if (v >= 1) c->chunk_blocks = v;
+    }
+    *out = c;
+  });
+}
+
+int mmi_ctx_destroy(mmi_ctx* ctx) {
+  return guarded([&] {
+    if (!ctx) fail(MMI_ERR_INVALID_ARG, "ctx is NULL");
+    (void)hipSetDevice(ctx->device);
+    (void)hipDeviceSynchronize();
+    if (ctx->pinned) (void)hipHostFree(ctx->pinned);
+    delete ctx;
+  });
+}
+
+int mmi_plan_create(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* cfgs, const void* q,
+                    const void* k, void* stream, mmi_plan** out) {
+  mmi_plan* P = nullptr;
+  int rc = guarded([&] {
+    validate_inputs(prob, cfgs, q, k);     // host-only checks first
+    if (!ctx || !out) fail(MMI_ERR_INVALID_ARG, "ctx/out is NULL");
+    P = new mmi_plan();
+    plan_create_impl(ctx, prob, cfgs, q, k, (hipStream_t)stream, P);
+  });
+  if (rc != MMI_OK) {
+    if (P) {
+      if (P->ctx) {
+        (void)hipStreamSynchronize((hipStream_t)stream);
+        free_plan_buffers(P);
+      }
+      delete P;
+    }
+    return rc;
+  }
+  *out = P;
+  return MMI_OK;
+}
+
+int mmi_plan_execute(mmi_plan* plan, const void* q, const void* k, const void* v, void* o, float* lse,
+                     void* stream) {
+  return guarded([&] {
+    if (!plan) fail(MMI_ERR_STATE, "plan is NULL");
+    plan_execute_impl(plan, q, k, v, o, lse, (hipStream_t)stream);
+  });
+}
+
+int mmi_plan_destroy(mmi_plan* plan) {
+  return guarded([&] {
+    if (!plan) fail(MMI_ERR_INVALID_ARG, "plan is NULL");
+    (void)hipSetDevice(plan->ctx->device);
+    HIPCHK(hipStreamSynchronize(plan->stream));
+    free_plan_buffers(plan);
+    delete plan;
+  });
+}
+
+int mmi_plan_stats(mmi_plan* P, int head, mmi_head_stats* out) {
+  return guarded([&] {
+    if (!P || !out) fail(MMI_ERR_INVALID_ARG, "plan/out is NULL");
+    if (head < 0 || head >= P->Hq) fail(MMI_ERR_INVALID_ARG, "head %d out of range", head);
+    HIPCHK(hipSetDevice(P->ctx->device));
+    HIPCHK(hipStreamSynchronize(P->stream));
+    const HostHead& H = P->hh[head];
+    const HeadDev& hd = P->heads[head];
+    mmi_head_stats s{};
+    s.kind = H.kind;
+    s.n_qblocks = hd.nbq;
+    s.n_kblocks = hd.nbk;
+    s.nnz_blocks = H.nnz;
+    const int64_t nb = (P->S + B - 1) / B;
+    s.causal_blocks = nb * (nb + 1) / 2;
+    s.split_rows = (int32_t)H.nsplit;
+    for (int i = 0; i < H.nops; ++i) {
+      const EstInfo& e = H.est[i];
+      if (e.params) {
+        int32_t prm[4];
+        HIPCHK(hipMemcpy(prm, e.params, sizeof prm, hipMemcpyDeviceToHost));
+        const int slot = H.op_slot[i];
+        if (slot < MMI_MAX_MODALITIES) { s.sigma[slot] = prm[0]; s.phase[slot] = prm[1]; }
+      }
+    }
+    *out = s;
+  });
+}
+
+int mmi_plan_export(mmi_plan* P, int head, int what, int slot, void* dst, size_t bytes, size_t* needed) {
+  return guarded([&] {
+    if (!P) fail(MMI_ERR_STATE, "plan is NULL");
+    if (head < 0 || head >= P->Hq) fail(MMI_ERR_INVALID_ARG, "head %d out of range", head);
+    HIPCHK(hipSetDevice(P->ctx->device));
+    HIPCHK(hipStreamSynchronize(P->stream));
+    const HostHead& H = P->hh[head];
+    const HeadDev& hd = P->heads[head];
+    const void* src = nullptr;
+    size_t n = 0;
+    std::vector<int32_t> tmp;
+    const EstInfo* e = nullptr;
+    if (what >= MMI_EXPORT_V_SCORES) {
+      for (int i = 0; i < H.nops; ++i)
+        if (H.op_slot[i] == slot) e = &H.est[i];
+      if (!e) fail(MMI_ERR_INVALID_ARG, "head %d has no op in slot %d", head, slot);
+    }
+    switch (what) {
+      case MMI_EXPORT_QPERM:
+      case MMI_EXPORT_KPERM: {
+        const int32_t* pm = what == MMI_EXPORT_QPERM ? hd.qperm : hd.kperm;
+        const int nslots = (what == MMI_EXPORT_QPERM ? hd.nbq : hd.nbk) * B;
+        n = (size_t)nslots * 4;
+        if (pm) {
+          src = pm;
+        } else {
+          tmp.resize(nslots);
+          for (int x = 0; x < nslots; ++x) tmp[x] = x < P->S ? x : -1;
+        }
+        break;
+      }
+      case MMI_EXPORT_ROW_PTR: src = hd.rowptr; n = (size_t)(hd.nbq + 1) * 4; break;
+      case MMI_EXPORT_COL_IDX: src = hd.col; n = (size_t)H.nnz * 4; break;
+      case MMI_EXPORT_V_SCORES: src = e->v; n = e->v ? (size_t)e->L_c * 4 : 0; break;
+      case MMI_EXPORT_U_SCORES: src = e->u; n = e->u ? (size_t)e->L_c * 4 : 0; break;
+      case MMI_EXPORT_FOLD: src = e->fold; n = e->fold ? (size_t)std::max(0, e->hi - e->lo + 1) * FOLD_W * 4 : 0; break;
+      case MMI_EXPORT_VSEL: src = e->vsel; n = (size_t)e->nv * 4; break;
+      case MMI_EXPORT_SSEL: src = e->ssel; n = (size_t)e->ns * 4; break;
+      case MMI_EXPORT_PARAMS: {
+        tmp.assign(4, 0);
+        if (e->params) HIPCHK(hipMemcpy(tmp.data(), e->params, 16, hipMemcpyDeviceToHost));
+        else { tmp[2] = e->L_c; tmp[3] = e->nrows; }
+        n = 16;
+        break;
+      }
+      case MMI_EXPORT_EST_LSE: {
+        if (e->rowset < 0) { n = 0; break; }
+        n = (size_t)e->nrows * 4;
+        std::vector<float> l2(e->nrows);
+        HIPCHK(hipMemcpy(l2.data(), P->est_lse2[e->rowset], n, hipMemcpyDeviceToHost));
+        tmp.resize(e->nrows);
+        for (int r = 0; r < e->nrows; ++r) {
+          const float x = l2[r] * LN2;
+          std::memcpy(&tmp[r], &x, 4);
+        }
+        break;
+      }
+      default: fail(MMI_ERR_INVALID_ARG, "unknown export kind %d", what);
+    }
+    if (needed) *needed = n;
+    if (!dst) return;
+    if (bytes < n) fail(MMI_ERR_INVALID_ARG, "destination holds %zu bytes, %zu needed", bytes, n);
+    if (n == 0) return;
+    if (!tmp.empty()) std::memcpy(dst, tmp.data(), n);
+    else HIPCHK(hipMemcpy(dst, src, n, hipMemcpyDeviceToHost));
+  });
+}
+
+int mmi_attention(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* cfgs, const void* q, const void* k,
+                  const void* v, void* o, float* lse, void* stream) {
+  mmi_plan* P = nullptr;
+  int rc = mmi_plan_create(ctx, prob, cfgs, q, k, stream, &P);
+  if (rc != MMI_OK) return rc;
+  rc = mmi_plan_execute(P, q, k, v, o, lse, stream);
+  const int rc2 = mmi_plan_destroy(P);
+  return rc != MMI_OK ? rc : rc2;
+}
+
+int mmi_dense_attention(mmi_ctx* ctx, const mmi_problem* prob, const void* q, const void* k, const void* v,
+                        void* o, float* lse, void* stream) {
+  if (!prob) {
+    g_last_error = "problem is NULL";
+    return MMI_ERR_INVALID_ARG;
+  }
+  if (prob->Hq < 1 || prob->Hq > (1 << 16)) {
+    g_last_error = "Hq out of range";
+    return MMI_ERR_INVALID_ARG;
+  }
+  std::vector<mmi_head_cfg> cfgs(prob->Hq);
+  for (auto& c : cfgs) {
+    std::memset(&c, 0, sizeof c);
+    c.kind = MMI_HEAD_GLOBAL;
+    c.global.kind = MMI_OP_DENSE;
+  }
+  return mmi_attention(ctx, prob, cfgs.data(), q, k, v, o, lse, stream);
+}
+
+int mmi_permute_rows(const void* src, int64_t src_stride, void* dst, int64_t dst_stride, const int32_t* perm,
+                     int64_t n_dst, int64_t row_bytes, void* stream) {
+  return guarded([&] {
+    if (!src || !dst || !perm) fail(MMI_ERR_INVALID_ARG, "NULL pointer");
+    if (n_dst < 0 || row_bytes <= 0 || row_bytes % 16 || src_stride % 16 || dst_stride % 16)
+      fail(MMI_ERR_INVALID_ARG, "rows and strides must be positive multiples of 16 bytes");
+    aligned16(src, "src"); aligned16(dst, "dst");
+    HIPCHK(launch_permute(src, src_stride, dst, dst_stride, perm, n_dst, row_bytes, 0, (hipStream_t)stream));
+  });
+}
+
+int mmi_unpermute_rows(const void* src, int64_t src_stride, void* dst, int64_t dst_stride, const int32_t* perm,
+                       int64_t n_src, int64_t row_bytes, void* stream) {
+  return guarded([&] {
+    if (!src || !dst || !perm) fail(MMI_ERR_INVALID_ARG, "NULL pointer");
+    if (n_src < 0 || row_bytes <= 0 || row_bytes % 16 || src_stride % 16 || dst_stride % 16)
+      fail(MMI_ERR_INVALID_ARG, "rows and strides must be positive multiples of 16 bytes");
+    aligned16(src, "src"); aligned16(dst, "dst");
+    HIPCHK(launch_permute(src, src_stride, dst, dst_stride, perm, n_src, row_bytes, 1, (hipStream_t)stream));
+  });
+}
+
+}  // extern "C"

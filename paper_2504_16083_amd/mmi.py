@@ -1,0 +1,266 @@
+"""ctypes binding of libmmi.so (include/mmi.h): argument marshalling only.
+
+Every function here converts Python/torch arguments to the C structs and
+device pointers of the C-ABI and calls the library; all computation runs in
+the HIP kernels. Loading fails loudly when libmmi.so has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as ct
+import os
+
+import numpy as np
+
+from synth import config as C
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmmi.so")
+
+MAXM = 8
+OK = 0
+EXPORT = dict(qperm=0, kperm=1, row_ptr=2, col_idx=3, v=4, u=5, fold=6, vsel=7, ssel=8, params=9, est_lse=10)
+_F32 = {"v", "u", "fold", "est_lse"}
+
+
+class MMIError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"mmi status {status}: {msg}")
+        self.status = status
+
+
+class mmi_op(ct.Structure):
+    _fields_ = [("kind", ct.c_int32), ("sink", ct.c_int32), ("local", ct.c_int32),
+                ("n_vertical", ct.c_int32), ("n_slash", ct.c_int32),
+                ("stride_lo", ct.c_int32), ("stride_hi", ct.c_int32),
+                ("use_h", ct.c_int32), ("use_v", ct.c_int32), ("use_s", ct.c_int32)]
+
+
+class mmi_head_cfg(ct.Structure):
+    _fields_ = [("kind", ct.c_int32), ("global_", mmi_op), ("intra", mmi_op * MAXM),
+                ("cross", (mmi_op * MAXM) * MAXM)]
+
+
+class mmi_problem(ct.Structure):
+    _fields_ = [("S", ct.c_int64), ("Hq", ct.c_int32), ("Hkv", ct.c_int32), ("D", ct.c_int32),
+                ("block", ct.c_int32),
+                ("q_stride_s", ct.c_int64), ("q_stride_h", ct.c_int64),
+                ("k_stride_s", ct.c_int64), ("k_stride_h", ct.c_int64),
+                ("v_stride_s", ct.c_int64), ("v_stride_h", ct.c_int64),
+                ("o_stride_s", ct.c_int64), ("o_stride_h", ct.c_int64),
+                ("modality", ct.POINTER(ct.c_uint8)), ("n_modalities", ct.c_int32)]
+
+
+class mmi_head_stats(ct.Structure):
+    _fields_ = [("kind", ct.c_int32), ("n_qblocks", ct.c_int32), ("n_kblocks", ct.c_int32),
+                ("nnz_blocks", ct.c_int64), ("causal_blocks", ct.c_int64), ("split_rows", ct.c_int32),
+                ("sigma", ct.c_int32 * MAXM), ("phase", ct.c_int32 * MAXM)]
+
+
+SYMBOLS = ["mmi_version", "mmi_status_str", "mmi_last_error", "mmi_ctx_create", "mmi_ctx_destroy",
+           "mmi_plan_create", "mmi_plan_execute", "mmi_plan_stats", "mmi_plan_export",
+           "mmi_plan_destroy", "mmi_attention", "mmi_dense_attention", "mmi_permute_rows",
+           "mmi_unpermute_rows"]
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run __graft_entry__.build() first")
+        L = ct.CDLL(LIB_PATH)
+        vp, i32, i64, sz = ct.c_void_p, ct.c_int, ct.c_int64, ct.c_size_t
+        sig = {
+            "mmi_version": ([], i32), "mmi_status_str": ([i32], ct.c_char_p),
+            "mmi_last_error": ([], ct.c_char_p),
+            "mmi_ctx_create": ([i32, ct.POINTER(vp)], i32), "mmi_ctx_destroy": ([vp], i32),
+            "mmi_plan_create": ([vp, ct.POINTER(mmi_problem), ct.POINTER(mmi_head_cfg), vp, vp, vp,
+                                 ct.POINTER(vp)], i32),
+            "mmi_plan_execute": ([vp, vp, vp, vp, vp, vp, vp], i32),
+            "mmi_plan_stats": ([vp, i32, ct.POINTER(mmi_head_stats)], i32),
+            "mmi_plan_export": ([vp, i32, i32, i32, vp, sz, ct.POINTER(sz)], i32),
+            "mmi_plan_destroy": ([vp], i32),
+            "mmi_attention": ([vp, ct.POINTER(mmi_problem), ct.POINTER(mmi_head_cfg), vp, vp, vp, vp, vp,
+                               vp], i32),
+            "mmi_dense_attention": ([vp, ct.POINTER(mmi_problem), vp, vp, vp, vp, vp, vp], i32),
+            "mmi_permute_rows": ([vp, i64, vp, i64, vp, i64, i64, vp], i32),
+            "mmi_unpermute_rows": ([vp, i64, vp, i64, vp, i64, i64, vp], i32),
+        }
+        for name, (args, res) in sig.items():
+            f = getattr(L, name)
+            f.argtypes, f.restype = args, res
+        _lib = L
+    return _lib
+
+
+def _check(status):
+    if status != OK:
+        raise MMIError(status, lib().mmi_last_error().decode(errors="replace"))
+
+
+def _ptr(t):
+    return None if t is None else ct.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return ct.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def mmi_version() -> int:
+    return lib().mmi_version()
+
+
+def mmi_status_str(s: int) -> str:
+    return lib().mmi_status_str(s).decode()
+
+
+def mmi_last_error() -> str:
+    return lib().mmi_last_error().decode(errors="replace")
+
+
+# ------------------------------------------------------------------ marshalling
+def op_struct(op: C.Op) -> mmi_op:
+    return mmi_op(op.kind, op.sink, op.local, op.n_vertical, op.n_slash, op.stride_lo, op.stride_hi,
+                  int(op.use_h), int(op.use_v), int(op.use_s))
+
+
+def head_cfgs(heads) -> ct.Array:
+    arr = (mmi_head_cfg * len(heads))()
+    for i, h in enumerate(heads):
+        c = arr[i]
+        c.kind = h.kind
+        c.global_ = op_struct(h.op)
+        for m in range(MAXM):
+            c.intra[m] = op_struct(h.intra_op(m))
+            for mk in range(MAXM):
+                c.cross[m][mk] = op_struct(h.cross_op(m, mk))
+    return arr
+
+
+class Problem:
+    """mmi_problem for packed [S, H, 128] tensors (or explicit strides)."""
+
+    def __init__(self, S, Hq, Hkv, modality=None, strides=None):
+        self.mod = None if modality is None else np.ascontiguousarray(modality, dtype=np.uint8)
+        p = mmi_problem()
+        p.S, p.Hq, p.Hkv, p.D, p.block = S, Hq, Hkv, 128, 64
+        for name, (ss, sh) in (strides or {}).items():
+            setattr(p, f"{name}_stride_s", ss)
+            setattr(p, f"{name}_stride_h", sh)
+        if self.mod is not None:
+            p.modality = self.mod.ctypes.data_as(ct.POINTER(ct.c_uint8))
+            p.n_modalities = int(self.mod.max()) + 1
+        self.c = p
+
+
+class Ctx:
+    def __init__(self, device: int = 0):
+        h = ct.c_void_p()
+        _check(lib().mmi_ctx_create(device, ct.byref(h)))
+        self.h = h
+
+    def close(self):
+        if self.h:
+            _check(lib().mmi_ctx_destroy(self.h))
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def mmi_ctx_create(device: int = 0) -> Ctx:
+    return Ctx(device)
+
+
+class Plan:
+    def __init__(self, ctx: Ctx, prob: Problem, heads, q, k, stream=None):
+        self.ctx, self.prob = ctx, prob
+        self.cfgs = head_cfgs(heads)
+        h = ct.c_void_p()
+        _check(lib().mmi_plan_create(ctx.h, ct.byref(prob.c), self.cfgs, _ptr(q), _ptr(k), _stream(stream),
+                                     ct.byref(h)))
+        self.h = h
+
+    def execute(self, q, k, v, o, lse=None, stream=None):
+        _check(lib().mmi_plan_execute(self.h, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _stream(stream)))
+
+    def stats(self, head: int) -> mmi_head_stats:
+        s = mmi_head_stats()
+        _check(lib().mmi_plan_stats(self.h, head, ct.byref(s)))
+        return s
+
+    def export(self, head: int, what: str, slot: int = 0) -> np.ndarray:
+        need = ct.c_size_t()
+        code = EXPORT[what]
+        _check(lib().mmi_plan_export(self.h, head, code, slot, None, 0, ct.byref(need)))
+        dt = np.float32 if what in _F32 else np.int32
+        out = np.zeros(need.value // 4, dtype=dt)
+        if need.value:
+            _check(lib().mmi_plan_export(self.h, head, code, slot, out.ctypes.data_as(ct.c_void_p), need.value,
+                                         ct.byref(need)))
+        return out
+
+    def destroy(self):
+        if self.h:
+            _check(lib().mmi_plan_destroy(self.h))
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def mmi_plan_create(ctx, prob, heads, q, k, stream=None) -> Plan:
+    return Plan(ctx, prob, heads, q, k, stream)
+
+
+def mmi_plan_execute(plan: Plan, q, k, v, o, lse=None, stream=None):
+    plan.execute(q, k, v, o, lse, stream)
+
+
+def mmi_plan_stats(plan: Plan, head: int):
+    return plan.stats(head)
+
+
+def mmi_plan_export(plan: Plan, head: int, what: str, slot: int = 0):
+    return plan.export(head, what, slot)
+
+
+def mmi_plan_destroy(plan: Plan):
+    plan.destroy()
+
+
+def mmi_attention(ctx, prob, heads, q, k, v, o, lse=None, stream=None):
+    cfgs = head_cfgs(heads)
+    _check(lib().mmi_attention(ctx.h, ct.byref(prob.c), cfgs, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
+                               _stream(stream)))
+
+
+def mmi_dense_attention(ctx, prob, q, k, v, o, lse=None, stream=None):
+    _check(lib().mmi_dense_attention(ctx.h, ct.byref(prob.c), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
+                                     _stream(stream)))
+
+
+def mmi_permute_rows(src, dst, perm, stream=None):
+    """dst[x] = src[perm[x]] row-wise (rows = first dim, contiguous rows)."""
+    rb = src[0].numel() * src.element_size()
+    _check(lib().mmi_permute_rows(_ptr(src), src.stride(0) * src.element_size(), _ptr(dst),
+                                  dst.stride(0) * dst.element_size(), _ptr(perm), perm.numel(), rb,
+                                  _stream(stream)))
+
+
+def mmi_unpermute_rows(src, dst, perm, stream=None):
+    """dst[perm[x]] = src[x] row-wise."""
+    rb = src[0].numel() * src.element_size()
+    _check(lib().mmi_unpermute_rows(_ptr(src), src.stride(0) * src.element_size(), _ptr(dst),
+                                    dst.stride(0) * dst.element_size(), _ptr(perm), perm.numel(), rb,
+                                    _stream(stream)))

@@ -1,0 +1,82 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/mmi.h declares, struct layouts agree, and host-side validation
+returns the documented status codes without touching a device."""
+import ctypes as ct
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2504_16083_amd import mmi
+from synth import config as C
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared():
+    src = open(os.path.join(ROOT, "include", "mmi.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(mmi_\w+)\s*\(", src, re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared()
+    assert len(names) == 14 and set(names) == set(mmi.SYMBOLS)
+    L = mmi.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert mmi.mmi_version() == 1
+    assert mmi.mmi_status_str(0) == "ok"
+    assert mmi.mmi_status_str(-3) == "bad head config"
+
+
+def test_struct_sizes_match_header():
+    # offsets of the trailing fields fix the layout of everything before them
+    assert ct.sizeof(mmi.mmi_op) == 40
+    assert ct.sizeof(mmi.mmi_head_cfg) == 4 + 40 + 8 * 40 + 64 * 40
+    assert mmi.mmi_problem.modality.offset == 88 and ct.sizeof(mmi.mmi_problem) == 104
+
+
+def _create(prob, heads, q=16, k=16):
+    cfgs = mmi.head_cfgs(heads)
+    h = ct.c_void_p()
+    return mmi.lib().mmi_plan_create(None, ct.byref(prob.c), cfgs, ct.c_void_p(q), ct.c_void_p(k), None,
+                                     ct.byref(h))
+
+
+def test_validation_codes_without_device():
+    g = [C.global_head(C.dense())] * 2
+    assert _create(mmi.Problem(100, 2, 1), g) == -1          # ctx NULL after valid args
+    p = mmi.Problem(100, 2, 1); p.c.D = 64
+    assert _create(p, g) == -2
+    assert _create(mmi.Problem(100, 3, 2), [C.global_head(C.dense())] * 3) == -2
+    assert _create(mmi.Problem(0, 2, 1), g) == -1
+    assert _create(mmi.Problem((1 << 21) + 1, 2, 1), g) == -2
+    assert _create(mmi.Problem(100, 2, 1), g, q=0) == -1
+    assert _create(mmi.Problem(100, 2, 1), g, q=8) == -1      # misaligned
+    assert _create(mmi.Problem(100, 2, 1), [C.global_head(C.grid(0, 5))] * 2) == -3
+    assert _create(mmi.Problem(100, 2, 1), [C.global_head(C.grid(5, 2000))] * 2) == -3
+    assert _create(mmi.Problem(100, 2, 1), [C.global_head(C.vert(5))] * 2) == -3
+    mod = np.zeros(100, np.uint8); mod[50:] = 1
+    assert _create(mmi.Problem(100, 2, 1, mod), [C.qboundary_head({1: C.grid(4, 8)})] * 2) == -3
+    bad2d = C.boundary2d_head({0: C.dense(), 1: C.dense()}, {(0, 1): C.ashape(1, 1)})
+    assert _create(mmi.Problem(100, 2, 1, mod), [bad2d] * 2) == -3
+    assert "cross" in mmi.mmi_last_error()
+    mod[3] = 9
+    p = mmi.Problem(100, 2, 1, mod); p.c.n_modalities = 2
+    assert _create(p, g) == -1
+
+
+def test_ctx_without_device_is_an_error():
+    h = ct.c_void_p()
+    rc = mmi.lib().mmi_ctx_create(0, ct.byref(h))
+    try:
+        import torch
+        has_gpu = torch.cuda.is_available()
+    except Exception:
+        has_gpu = False
+    if has_gpu:
+        assert rc == 0
+        mmi.lib().mmi_ctx_destroy(h)
+    else:
+        assert rc in (-1, -5) and mmi.mmi_last_error()

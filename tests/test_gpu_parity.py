@@ -1,0 +1,121 @@
+"""HIP path vs oracle through the C-ABI (needs an MI355X)."""
+import numpy as np
+import pytest
+import torch
+
+from synth import config as C
+from synth import generate, workloads
+
+from parity import full_check, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    from paper_2504_16083_amd import mmi
+    c = mmi.Ctx(0)
+    yield c
+    c.close()
+
+
+def _rand_qkv(S, Hq, Hkv, seed, scale_k=1.0):
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn(S, Hq, 128, generator=g)
+    k = torch.randn(S, Hkv, 128, generator=g) * scale_k
+    v = torch.randn(S, Hkv, 128, generator=g)
+    return [t.to(torch.bfloat16).cuda() for t in (q, k, v)]
+
+
+@pytest.mark.parametrize("S", [64, 200, 1000, 4096 + 37])
+def test_dense_small(ctx, S):
+    say(f"[gpu] dense S={S}")
+    q, k, v = _rand_qkv(S, 2, 1, seed=S)
+    heads = [C.global_head(C.dense())] * 2
+    rep = full_check(ctx, S, 2, 1, None, heads, q, k, v)
+    say(f"  max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g}")
+
+
+def test_config0_grid(ctx):
+    say("[gpu] config0 grid 4096")
+    wl = workloads.config0()
+    q, k, v = generate.make_qkv(wl, "cpu")
+    q, k, v = q.cuda(), k.cuda(), v.cuda()
+    rep = full_check(ctx, wl.S, wl.Hq, wl.Hkv, wl.modality, wl.heads, q, k, v)
+    assert not rep.ties
+    assert all(n == 206 for n in rep.nnz.values()), rep.nnz
+    say(f"  nnz={rep.nnz} max|dO|={rep.max_o:.3g}")
+
+
+@pytest.mark.parametrize("kind", ["ashape", "vslash", "grid_window", "grid_lines"])
+def test_global_ops_small(ctx, kind):
+    say(f"[gpu] global op {kind}")
+    S = 2500
+    q, k, v = _rand_qkv(S, 2, 1, seed=7, scale_k=2.0)
+    op = {"ashape": C.ashape(64, 300), "vslash": C.vslash(40, 30),
+          "grid_window": C.grid(50, 70), "grid_lines": C.grid(30, 31, True, True, False)}[kind]
+    rep = full_check(ctx, S, 2, 1, None, [C.global_head(op)] * 2, q, k, v)
+    say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
+
+
+def _mm_layout(S, seed):
+    rng = np.random.default_rng(seed)
+    mod = np.zeros(S, np.uint8)
+    pos, m = 0, 0
+    while pos < S:
+        n = int(rng.integers(50, 700))
+        mod[pos:pos + n] = m
+        pos += n
+        m ^= 1
+    return mod
+
+
+def test_boundary_heads_small(ctx):
+    say("[gpu] boundary heads")
+    S = 3000
+    mod = _mm_layout(S, 3)
+    q, k, v = _rand_qkv(S, 4, 2, seed=11, scale_k=2.0)
+    heads = [
+        C.qboundary_head({0: C.ashape(32, 200), 1: C.vslash(30, 20)}),
+        C.boundary2d_head({0: C.ashape(32, 200), 1: C.grid(20, 40)}, {(0, 1): C.vert(40), (1, 0): C.dense()}),
+        C.boundary2d_head({0: C.vslash(20, 20), 1: C.dense()}, {(0, 1): C.dense(), (1, 0): C.none()}),
+        C.qboundary_head({0: C.dense(), 1: C.ashape(0, 128)}),
+    ]
+    rep = full_check(ctx, S, 4, 2, mod, heads, q, k, v)
+    say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
+
+
+def test_determinism(ctx):
+    say("[gpu] determinism")
+    from paper_2504_16083_amd import mmi
+    wl = workloads.config0()
+    q, k, v = (t.cuda() for t in generate.make_qkv(wl, "cpu"))
+    outs = []
+    for _ in range(2):
+        prob = mmi.Problem(wl.S, wl.Hq, wl.Hkv, wl.modality)
+        o = torch.empty_like(q)
+        lse = torch.empty(wl.Hq, wl.S, device="cuda")
+        plan = mmi.Plan(ctx, prob, wl.heads, q, k)
+        plan.execute(q, k, v, o, lse)
+        torch.cuda.synchronize()
+        outs.append((o.clone(), lse.clone(), plan.export(0, "col_idx"), plan.export(0, "v")))
+        plan.destroy()
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+    assert np.array_equal(outs[0][2], outs[1][2]) and np.array_equal(outs[0][3], outs[1][3])
+
+
+def test_permute_roundtrip(ctx):
+    say("[gpu] permute/unpermute")
+    from paper_2504_16083_amd import mmi
+    S = 5000
+    x = torch.randn(S, 4, 128, device="cuda").to(torch.bfloat16)
+    perm = torch.randperm(S, device="cuda").to(torch.int32)
+    perm = torch.cat([perm, torch.full((40,), -1, device="cuda", dtype=torch.int32)])
+    y = torch.empty(S + 40, 4, 128, device="cuda", dtype=torch.bfloat16)
+    mmi.mmi_permute_rows(x, y, perm)
+    z = torch.zeros_like(x)
+    mmi.mmi_unpermute_rows(y, z, perm)
+    torch.cuda.synchronize()
+    assert torch.equal(y[:S], x[perm[:S].long()])
+    assert torch.count_nonzero(y[S:]) == 0
+    assert torch.equal(z, x)
