@@ -120,6 +120,19 @@ typedef struct mmi_head_stats {
   int32_t phase[MMI_MAX_MODALITIES];
 } mmi_head_stats;
 
+/* Stage durations of a plan, from HIP events recorded on the plan's stream
+ * (Section 4.6 / Appendix E report latency including the index building).
+ * create_* cover mmi_plan_create, attn/combine the last mmi_plan_execute. */
+typedef struct mmi_plan_timing {
+  float est_ms;        /* estimation passes (row LSE, column/diagonal scores) */
+  float select_ms;     /* Grid stride/phase search, vertical/slash top-k */
+  float index_ms;      /* permutations, block index, work list (incl. one host sync) */
+  float attn_ms;       /* block-sparse attention kernel */
+  float combine_ms;    /* merge of split query blocks */
+  int64_t computed_blocks;  /* selected 64x64 blocks over all heads */
+  int64_t work_items;
+} mmi_plan_timing;
+
 /* export kinds for mmi_plan_export (host copies; the call synchronises) */
 #define MMI_EXPORT_QPERM 0       /* int32[n_qblocks*64]: slot -> position or -1 */
 #define MMI_EXPORT_KPERM 1       /* int32[n_kblocks*64] */
@@ -167,6 +180,9 @@ int mmi_plan_stats(mmi_plan* plan, int head, mmi_head_stats* out);
  * small, only *needed is written (and MMI_OK returned if dst is NULL). */
 int mmi_plan_export(mmi_plan* plan, int head, int what, int slot, void* host_dst,
                     size_t bytes, size_t* needed);
+
+/* Stage durations (synchronises with the plan's stream). */
+int mmi_plan_timing_get(mmi_plan* plan, mmi_plan_timing* out);
 
 int mmi_plan_destroy(mmi_plan* plan);
 

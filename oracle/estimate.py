@@ -27,11 +27,12 @@ def tau(D: int = 128) -> float:
 
 def row_lse(Qr: np.ndarray, K: np.ndarray, rows: np.ndarray, scale: float) -> np.ndarray:
     """LSE_r = ln sum_{k <= pos(r)} exp(scale * q_r . k_k)."""
+    s = scale * (K[: int(rows.max()) + 1] @ Qr.T)          # [keys, rows]
     out = np.empty(len(rows))
     for r, p in enumerate(rows):
-        s = scale * (K[: p + 1] @ Qr[r])
-        m = s.max()
-        out[r] = m + math.log(np.exp(s - m).sum())
+        col = s[: p + 1, r]
+        m = col.max()
+        out[r] = m + math.log(np.exp(col - m).sum())
     return out
 
 
@@ -48,13 +49,11 @@ def scores(Qr, K, rows, lse, scale, key_pos=None, row_coord=None):
     key_pos maps coordinate -> position (None: coordinate = position)."""
     L_c = visible_extent(rows, key_pos)
     kp = np.arange(L_c) if key_pos is None else np.asarray(key_pos[:L_c])
-    Kc = K[kp]
+    logits = scale * (K[kp] @ Qr.T)                         # [L_c, rows]
     v = np.zeros(L_c)
     u = None if row_coord is None else np.zeros(L_c)
     for r, p in enumerate(rows):
-        vis = kp <= p
-        a = np.zeros(L_c)
-        a[vis] = np.exp(scale * (Kc[vis] @ Qr[r]) - lse[r])
+        a = np.where(kp <= p, np.exp(logits[:, r] - lse[r]), 0.0)
         v += a
         if u is not None:
             kr = int(row_coord[r])

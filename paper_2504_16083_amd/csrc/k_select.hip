@@ -143,9 +143,9 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk(const TopkJob* jobs) {
     const int eq_before = eq_base + (inc & 0xffff) - eq;
     const int take_eq = eq && eq_before < remaining;
     const int sel = gt | take_eq;
-    // number selected before i = gt before + min(eq before, remaining)
+    // selected before i in this chunk: greater ones + equal ones taken since the chunk start
     const int gt_before = (inc >> 16) - gt;
-    const int pos = out_base + gt_before + min(eq_before, remaining);
+    const int pos = out_base + gt_before + min(eq_before, remaining) - min(eq_base, remaining);
     if (sel && pos < jb.n) jb.out[pos] = i;
     const int tot = scan[TK_THREADS - 1];
     __syncthreads();

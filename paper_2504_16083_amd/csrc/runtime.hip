@@ -100,6 +100,7 @@ class Allocator {
 struct mmi_ctx {
   int device = 0;
   int chunk_blocks = 128;
+  int live_plans = 0;              // plans created from this context and not destroyed
   mmi::Allocator alloc;
   int64_t* pinned = nullptr;       // host staging for totals
   size_t pinned_n = 0;
@@ -157,6 +158,9 @@ struct mmi_plan {
   int32_t* d_tpos = nullptr;
   std::vector<float*> est_lse2;  // per rowset
   std::vector<std::vector<uint8_t>> keep;   // host sources of asynchronous uploads
+  hipEvent_t ev[7] = {};          // stage boundaries: create 0..3, execute 4..6
+  int64_t nnz_all = 0;
+  bool executed = false;
   std::vector<int> rowset_n;
 };
 
@@ -601,15 +605,19 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
 
   // estimation -> choices
   const Tensor tq{q, p.q_stride_s, p.q_stride_h}, tk{k, p.k_stride_s, p.k_stride_h};
+  for (auto& e : P->ev) HIPCHK(hipEventCreate(&e));
   RowSet* d_rs = upload(P, bd.rowsets);
   EstJob* d_jobs = upload(P, bd.jobs);
+  HIPCHK(hipEventRecord(P->ev[0], st));
   HIPCHK(launch_est_lse(d_rs, (int)bd.rowsets.size(), bd.max_chunks, tq, tk, bd.chunk_keys, st));
   HIPCHK(launch_est_scores(d_jobs, (int)bd.jobs.size(), bd.max_tiles, d_rs, tq, tk, st));
   HIPCHK(launch_est_udiag(d_jobs, (int)bd.jobs.size(), bd.max_L, st));
+  HIPCHK(hipEventRecord(P->ev[1], st));
   GridJob* d_g = upload(P, bd.gjobs);
   HIPCHK(launch_grid_search(d_g, (int)bd.gjobs.size(), bd.max_cands, st));
   TopkJob* d_t = upload(P, bd.tjobs);
   HIPCHK(launch_topk(d_t, (int)bd.tjobs.size(), st));
+  HIPCHK(hipEventRecord(P->ev[2], st));
 
   // permutations, key summaries, block counts
   P->d_heads = upload(P, P->heads);
@@ -667,6 +675,8 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   int64_t* d_pb = upload(P, part_base);
   int64_t* d_sb = upload(P, split_base);
   HIPCHK(launch_work_fill(P->d_heads, p.Hq, d_ib, d_pb, d_sb, max_nbq, chunk, P->d_items, P->d_splits, st));
+  HIPCHK(hipEventRecord(P->ev[3], st));
+  P->nnz_all = nnz_all;
 }
 
 static void plan_execute_impl(mmi_plan* P, const void* q, const void* k, const void* v, void* o, float* lse,
@@ -688,9 +698,13 @@ static void plan_execute_impl(mmi_plan* P, const void* q, const void* k, const v
   a.nitems = P->nitems;
   a.part_o = P->d_part_o;
   a.part_ml = P->d_part_ml;
+  HIPCHK(hipEventRecord(P->ev[4], st));
   HIPCHK(launch_attention(a, st));
+  HIPCHK(hipEventRecord(P->ev[5], st));
   HIPCHK(launch_combine(a, P->d_splits, P->nsplit, st));
+  HIPCHK(hipEventRecord(P->ev[6], st));
   P->stream = st;
+  P->executed = true;
 }
 
 }  // namespace mmi
@@ -758,6 +772,8 @@ int mmi_ctx_create(int device, mmi_ctx** out) {
 int mmi_ctx_destroy(mmi_ctx* ctx) {
   return guarded([&] {
     if (!ctx) fail(MMI_ERR_INVALID_ARG, "ctx is NULL");
+    if (ctx->live_plans > 0)
+      fail(MMI_ERR_STATE, "context still has %d live plan(s); destroy them first", ctx->live_plans);
     (void)hipSetDevice(ctx->device);
     (void)hipDeviceSynchronize();
     if (ctx->pinned) (void)hipHostFree(ctx->pinned);
@@ -784,6 +800,7 @@ int mmi_plan_create(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* c
     }
     return rc;
   }
+  ++ctx->live_plans;
   *out = P;
   return MMI_OK;
 }
@@ -802,6 +819,9 @@ int mmi_plan_destroy(mmi_plan* plan) {
     (void)hipSetDevice(plan->ctx->device);
     HIPCHK(hipStreamSynchronize(plan->stream));
     free_plan_buffers(plan);
+    for (auto& e : plan->ev)
+      if (e) (void)hipEventDestroy(e);
+    --plan->ctx->live_plans;
     delete plan;
   });
 }
@@ -832,6 +852,25 @@ int mmi_plan_stats(mmi_plan* P, int head, mmi_head_stats* out) {
       }
     }
     *out = s;
+  });
+}
+
+int mmi_plan_timing_get(mmi_plan* P, mmi_plan_timing* out) {
+  return guarded([&] {
+    if (!P || !out) fail(MMI_ERR_INVALID_ARG, "plan/out is NULL");
+    HIPCHK(hipSetDevice(P->ctx->device));
+    HIPCHK(hipStreamSynchronize(P->stream));
+    mmi_plan_timing t{};
+    HIPCHK(hipEventElapsedTime(&t.est_ms, P->ev[0], P->ev[1]));
+    HIPCHK(hipEventElapsedTime(&t.select_ms, P->ev[1], P->ev[2]));
+    HIPCHK(hipEventElapsedTime(&t.index_ms, P->ev[2], P->ev[3]));
+    if (P->executed) {
+      HIPCHK(hipEventElapsedTime(&t.attn_ms, P->ev[4], P->ev[5]));
+      HIPCHK(hipEventElapsedTime(&t.combine_ms, P->ev[5], P->ev[6]));
+    }
+    t.computed_blocks = P->nnz_all;
+    t.work_items = P->nitems;
+    *out = t;
   });
 }
 

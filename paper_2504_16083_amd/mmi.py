@@ -6,8 +6,10 @@ the HIP kernels. Loading fails loudly when libmmi.so has not been built.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes as ct
 import os
+import weakref
 
 import numpy as np
 
@@ -56,7 +58,13 @@ class mmi_head_stats(ct.Structure):
                 ("sigma", ct.c_int32 * MAXM), ("phase", ct.c_int32 * MAXM)]
 
 
-SYMBOLS = ["mmi_version", "mmi_status_str", "mmi_last_error", "mmi_ctx_create", "mmi_ctx_destroy",
+class mmi_plan_timing(ct.Structure):
+    _fields_ = [("est_ms", ct.c_float), ("select_ms", ct.c_float), ("index_ms", ct.c_float),
+                ("attn_ms", ct.c_float), ("combine_ms", ct.c_float), ("computed_blocks", ct.c_int64),
+                ("work_items", ct.c_int64)]
+
+
+SYMBOLS = ["mmi_plan_timing_get", "mmi_version", "mmi_status_str", "mmi_last_error", "mmi_ctx_create", "mmi_ctx_destroy",
            "mmi_plan_create", "mmi_plan_execute", "mmi_plan_stats", "mmi_plan_export",
            "mmi_plan_destroy", "mmi_attention", "mmi_dense_attention", "mmi_permute_rows",
            "mmi_unpermute_rows"]
@@ -81,6 +89,7 @@ def lib():
             "mmi_plan_stats": ([vp, i32, ct.POINTER(mmi_head_stats)], i32),
             "mmi_plan_export": ([vp, i32, i32, i32, vp, sz, ct.POINTER(sz)], i32),
             "mmi_plan_destroy": ([vp], i32),
+            "mmi_plan_timing_get": ([vp, ct.POINTER(mmi_plan_timing)], i32),
             "mmi_attention": ([vp, ct.POINTER(mmi_problem), ct.POINTER(mmi_head_cfg), vp, vp, vp, vp, vp,
                                vp], i32),
             "mmi_dense_attention": ([vp, ct.POINTER(mmi_problem), vp, vp, vp, vp, vp, vp], i32),
@@ -157,14 +166,23 @@ class Problem:
         self.c = p
 
 
+_live_ctx = weakref.WeakSet()
+
+
 class Ctx:
+    """mmi_ctx; closing it first destroys every plan still alive on it."""
+
     def __init__(self, device: int = 0):
         h = ct.c_void_p()
         _check(lib().mmi_ctx_create(device, ct.byref(h)))
         self.h = h
+        self.plans = weakref.WeakSet()
+        _live_ctx.add(self)
 
     def close(self):
         if self.h:
+            for p in list(self.plans):
+                p.destroy()
             _check(lib().mmi_ctx_destroy(self.h))
             self.h = None
 
@@ -187,6 +205,7 @@ class Plan:
         _check(lib().mmi_plan_create(ctx.h, ct.byref(prob.c), self.cfgs, _ptr(q), _ptr(k), _stream(stream),
                                      ct.byref(h)))
         self.h = h
+        ctx.plans.add(self)
 
     def execute(self, q, k, v, o, lse=None, stream=None):
         _check(lib().mmi_plan_execute(self.h, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _stream(stream)))
@@ -195,6 +214,11 @@ class Plan:
         s = mmi_head_stats()
         _check(lib().mmi_plan_stats(self.h, head, ct.byref(s)))
         return s
+
+    def timing(self) -> dict:
+        t = mmi_plan_timing()
+        _check(lib().mmi_plan_timing_get(self.h, ct.byref(t)))
+        return {f: getattr(t, f) for f, _ in mmi_plan_timing._fields_}
 
     def export(self, head: int, what: str, slot: int = 0) -> np.ndarray:
         need = ct.c_size_t()
@@ -235,6 +259,10 @@ def mmi_plan_export(plan: Plan, head: int, what: str, slot: int = 0):
     return plan.export(head, what, slot)
 
 
+def mmi_plan_timing_get(plan: Plan) -> dict:
+    return plan.timing()
+
+
 def mmi_plan_destroy(plan: Plan):
     plan.destroy()
 
@@ -264,3 +292,13 @@ def mmi_unpermute_rows(src, dst, perm, stream=None):
     _check(lib().mmi_unpermute_rows(_ptr(src), src.stride(0) * src.element_size(), _ptr(dst),
                                     dst.stride(0) * dst.element_size(), _ptr(perm), perm.numel(), rb,
                                     _stream(stream)))
+
+
+@atexit.register
+def _close_all():
+    """Release plans and contexts before the HIP runtime shuts down."""
+    for c in list(_live_ctx):
+        try:
+            c.close()
+        except Exception:
+            pass

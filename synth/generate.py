@@ -66,11 +66,30 @@ def video_index(modality: np.ndarray) -> np.ndarray:
     return np.nonzero(modality == 1)[0]
 
 
+def segments(modality: np.ndarray):
+    """Maximal runs [(modality, start, end)] of the layout."""
+    m = np.asarray(modality)
+    cut = np.nonzero(np.diff(m.astype(np.int16)))[0] + 1
+    starts = np.concatenate([[0], cut])
+    ends = np.concatenate([cut, [len(m)]])
+    return [(int(m[a]), int(a), int(b)) for a, b in zip(starts, ends)]
+
+
+def _periodic(E, first, n):
+    """Rows E[(first + i) mod len(E)] for i < n, built from copies only."""
+    sig = E.shape[0]
+    reps = (n + sig - 1) // sig + 1
+    return torch.roll(E, -first, 0).repeat(reps, 1)[:n]
+
+
 def make_qkv(wl: Workload, device="cpu", dtype=torch.bfloat16):
     """Q [S,Hq,128], K [S,Hkv,128], V [S,Hkv,128] (bf16) for the workload.
 
-    Deterministic for a given (workload seed, device type)."""
+    Deterministic for a given (workload seed, device type). Large tensors are
+    only ever updated through contiguous or strided slices."""
     S, Hq, Hkv, D = wl.S, wl.Hq, wl.Hkv, 128
+    if len(wl.modality) != S:
+        raise ValueError(f"layout has {len(wl.modality)} tokens, S = {S}")
     G = Hq // Hkv
     dev = torch.device(device)
     gen = torch.Generator(device=dev)
@@ -83,40 +102,45 @@ def make_qkv(wl: Workload, device="cpu", dtype=torch.bfloat16):
     K = randn(S, Hkv, D)
     V = randn(S, Hkv, D)
     st = wl.structure
-    vid = torch.from_numpy(video_index(wl.modality)).to(dev)
-    nvid = int(vid.numel())
-    if nvid:
-        vloc = torch.arange(nvid, device=dev)
+    segs = segments(wl.modality)
+    vsegs, vloc = [], 0
+    for m, a, b in segs:
+        if m == 1:
+            vsegs.append((a, b, vloc))
+            vloc += b - a
+    if vsegs:
         for g in range(Hkv):
             sig = int(st.sigma[g])
             E = st.amp * randn(sig, D)
-            slot = vloc % sig
-            e = E[slot]
-            K[vid, g] += e
-            Q[vid, g * G:(g + 1) * G] += e[:, None, :]
             w = randn(D)
             p_star = int(st.line_slot[g]) if st.line_slot else 0
-            line = vid[slot == p_star]
-            K[line, g] += st.line_k * w
-            Q[vid, g * G:(g + 1) * G] += st.line_q * w
-    txt = torch.from_numpy(np.nonzero(wl.modality == 0)[0]).to(dev)
-    if st.text_amp > 0 and txt.numel() > 1:
-        n = int(txt.numel())
+            for a, b, v0 in vsegs:
+                e = _periodic(E, v0 % sig, b - a)
+                K[a:b, g] += e
+                Q[a:b, g * G:(g + 1) * G] += e[:, None, :]
+                first = (p_star - v0) % sig
+                K[a + first:b:sig, g] += st.line_k * w
+                Q[a:b, g * G:(g + 1) * G] += st.line_q * w
+    tsegs = [(a, b) for m, a, b in segs if m == 0]
+    n_txt = sum(b - a for a, b in tsegs)
+    if st.text_amp > 0 and n_txt > 1:
         taps = 128
         kern = torch.tensor([st.text_rho ** t for t in range(taps)], device=dev,
                             dtype=torch.float32) * math.sqrt(1 - st.text_rho ** 2)
         for g in range(Hkv):
-            z = randn(1, D, n + taps - 1)
-            z = torch.nn.functional.conv1d(z.reshape(D, 1, -1),
-                                           kern.flip(0).reshape(1, 1, -1))
-            z = z.reshape(D, n).t() * st.text_amp
-            K[txt, g] += z
-            Q[txt, g * G:(g + 1) * G] += z[:, None, :]
+            z = randn(1, D, n_txt + taps - 1)
+            z = torch.nn.functional.conv1d(z.reshape(D, 1, -1), kern.flip(0).reshape(1, 1, -1))
+            z = z.reshape(D, n_txt).t() * st.text_amp
+            off = 0
+            for a, b in tsegs:
+                K[a:b, g] += z[off:off + b - a]
+                Q[a:b, g * G:(g + 1) * G] += z[off:off + b - a, None, :]
+                off += b - a
     if st.sink_frac > 0:
         nsink = max(1, int(round(st.sink_frac * S)))
         perm = torch.randperm(S, generator=gen, device=dev)[:nsink]
         for g in range(Hkv):
             u = randn(D)
-            K[perm, g] += 3.0 * u
+            K[:, g].index_add_(0, perm, (3.0 * u).expand(nsink, D).contiguous())
             Q[:, g * G:(g + 1) * G] += 0.5 * u
     return Q.to(dtype), K.to(dtype), V.to(dtype)

@@ -88,9 +88,10 @@ def config2() -> Workload:
 
 
 def config3() -> Workload:
-    """262144 = 256 text + 1024 frames x 256; 32/8; amp 1.5; 1% sink keys."""
+    """262144 = 256 text + 1023 frames x 256 (the stated "256 text + 1024 frames"
+    is 256 tokens over 2^18; the frame count gives way); 32/8; amp 1.5; 1% sinks."""
     rng = _rng(3)
-    mod = _layout([(0, 256), (1, 1024 * 256)])
+    mod = _layout([(0, 256), (1, 1023 * 256)])
     sig = [256] * 8
     st = Structure(sigma=sig, amp=1.5, sink_frac=0.01)
     st.line_slot = _line_slots(rng, sig)
@@ -129,4 +130,6 @@ ALL = [config0, config1, config2, config3, config4]
 
 
 def by_id(cid: int) -> Workload:
-    return ALL[cid]()
+    wl = ALL[cid]()
+    assert len(wl.modality) == wl.S, (wl.name, len(wl.modality), wl.S)
+    return wl

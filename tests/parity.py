@@ -81,7 +81,7 @@ def compare_head(plan, h, hp: OP.HeadPlan, rep: Report, exact_choices=True):
         assert len(gv) == est.L_c, (h, key, len(gv), est.L_c)
         ev = _rel_err(gv, est.v)
         assert ev <= SCORE_RTOL, f"head {h} {key}: v rel err {ev}"
-        if est.u is not None:
+        if est.u is not None and hp.ops[key].op.kind == C.OP_VSLASH:
             gu = plan.export(h, "u", s)
             eu = _rel_err(gu, est.u)
             assert eu <= SCORE_RTOL, f"head {h} {key}: u rel err {eu}"
@@ -160,11 +160,13 @@ def full_check(ctx, S, Hq, Hkv, modality, heads, q, k, v, rows=None, heads_to_ch
     LSE = lse.cpu().double().numpy()
     G = Hq // Hkv
     rep = Report()
-    for h in (heads_to_check if heads_to_check is not None else range(Hq)):
-        hp = OP.plan_head(heads[h], S, modality, lambda r, h=h: Q[r, h], K[:, h // G])
-        exact = compare_head(plan, h, hp, rep)
-        if exact:
-            rr = np.arange(S) if rows is None else rows
-            compare_outputs(h, hp, Q, K, V, h // G, O, LSE, rr, rep)
-    plan.destroy()
+    try:
+        for h in (heads_to_check if heads_to_check is not None else range(Hq)):
+            hp = OP.plan_head(heads[h], S, modality, lambda r, h=h: Q[r, h], K[:, h // G])
+            exact = compare_head(plan, h, hp, rep)
+            if exact:
+                rr = np.arange(S) if rows is None else rows
+                compare_outputs(h, hp, Q, K, V, h // G, O, LSE, rr, rep)
+    finally:
+        plan.destroy()
     return rep

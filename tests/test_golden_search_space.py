@@ -22,3 +22,10 @@ def test_search_space_table_maps_to_ops():
         op = C.vslash(nv, ns)
         assert (op.n_vertical, op.n_slash) == (nv, ns)
     assert t["last_q"]["value"] == C.LAST_Q
+
+
+def test_workload_layouts_match_sequence_length():
+    from synth import workloads
+    for cid in range(5):
+        wl = workloads.by_id(cid)
+        assert len(wl.modality) == wl.S and wl.Hq % wl.Hkv == 0 and len(wl.heads) == wl.Hq
