@@ -88,16 +88,24 @@ struct HeadDev {
   int32_t* qperm;             // [nbq*64] or nullptr (identity)
   int32_t* kperm;             // [nbk*64] or nullptr (identity)
   int32_t* kminpos;           // [nbk] smallest key position per key block
+  int32_t* kmaxpos;           // [nbk] largest key position per key block (INT_BIG if it holds padding)
   int32_t* counts;            // [nbq]
   int32_t* rowptr;            // [nbq+1]
   uint32_t* bitmap;           // [nbq][nwords]
   int32_t nwords;
   int32_t* col;               // [nnz]
   int32_t op0;                // first OpDev of this head
-  int32_t* chunks;            // [nbq] work items per row
-  int32_t* itembase;          // [nbq] exclusive prefix of chunks
-  int32_t* splitoff;          // [nbq] exclusive prefix of (chunks > 1)
-  int32_t* partoff;           // [nbq] exclusive prefix of chunks over split rows
+  // Row groups: R consecutive query blocks processed by one work item over the
+  // union of their key lists (entries: key block | flags << 16, bit r of the
+  // flags = query block r of the group selects that key block).
+  int32_t ngroups;
+  int32_t* gcount;            // [ngroups] union sizes
+  int32_t* growptr;           // [ngroups+1]
+  int32_t* gcol;              // [gnnz]
+  int32_t* chunks;            // [ngroups] work items per group
+  int32_t* itembase;          // [ngroups] exclusive prefix of chunks
+  int32_t* splitoff;          // [ngroups] exclusive prefix of (chunks > 1)
+  int32_t* partoff;           // [ngroups] exclusive prefix of chunks over split groups
 };
 
 // group table (modalities present, ascending); identical for every boundary head
@@ -110,13 +118,13 @@ struct Groups {
 };
 
 struct WorkItem {
-  int32_t head, qblk, e0, e1;
+  int32_t head, group, e0, e1;   // union entries [e0, e1) of row group `group`
   int32_t part;       // -1: write O directly; else partial slot
   int32_t pad[3];
 };
 
-struct SplitRow {
-  int32_t head, qblk, part0, nparts;
+struct SplitRow {     // a row group whose union list is split over several items
+  int32_t head, group, part0, nparts;
 };
 
 // ---------------------------------------------------------------- launches
@@ -137,14 +145,17 @@ hipError_t launch_topk(const TopkJob* jobs, int njobs, hipStream_t st);
 // k_blocks.hip
 hipError_t launch_key_summaries(const HeadDev* heads, int nheads, OpDev* ops, int nops,
                                 Groups g, int max_nbk, int max_sel, hipStream_t st);
-hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* ops, Groups g,
-                               const int32_t* tpos, const Segment* segs, int nseg, int max_nbq,
-                               int chunk_blocks, hipStream_t st);
-// totals[head] = {nnz, nitems, nsplit, nparts}
+hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* ops, Groups g, int max_nbq,
+                               hipStream_t st);
+hipError_t launch_group_count(const HeadDev* heads, int nheads, int R, int max_groups, int chunk_blocks,
+                              hipStream_t st);
+// totals[head] = {nnz, gnnz, nitems, nsplit, nparts}
+constexpr int NTOT = 5;
 hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int64_t* totals, hipStream_t st);
-hipError_t launch_blocks_fill(const HeadDev* heads, int nheads, int max_nbq, hipStream_t st);
+hipError_t launch_blocks_fill(const HeadDev* heads, int nheads, int max_nbq, int R, int max_groups,
+                              hipStream_t st);
 hipError_t launch_work_fill(const HeadDev* heads, int nheads, const int64_t* item_base,
-                            const int64_t* part_base, const int64_t* split_base, int max_nbq,
+                            const int64_t* part_base, const int64_t* split_base, int max_groups,
                             int chunk_blocks, WorkItem* items, SplitRow* splits, hipStream_t st);
 // k_attention.hip
 struct AttnArgs {
@@ -155,8 +166,9 @@ struct AttnArgs {
   const HeadDev* heads;
   const WorkItem* items;
   int64_t nitems;
-  float* part_o;              // [nparts][64][128]
-  float* part_ml;             // [nparts][64][2]
+  float* part_o;              // [nparts][R*64][128]
+  float* part_ml;             // [nparts][R*64][2]
+  int32_t R;                  // query blocks per row group (1, 2 or 4)
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
 hipError_t launch_combine(const AttnArgs& a, const SplitRow* splits, int64_t nsplit, hipStream_t st);

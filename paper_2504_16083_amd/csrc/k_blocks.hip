@@ -11,11 +11,14 @@
 //   blocks in an LDS bitmap with closed-form rules (ranges, per-block
 //   threshold tests, slash offsets), then stores the bitmap and its
 //   popcount. Bit setting is an OR, so the result is order independent.
-// k_blocks_scan: per head, prefix sums of counts (CSR row pointers) and of
-//   work-item counts.
+// k_group_count / k_group_fill: the union of the key-block sets of R
+//   consecutive query blocks, with a per-query-block flag on every entry
+//   (the attention kernel loads each key block once for all R query blocks).
+// k_blocks_scan: per head, prefix sums of counts (CSR row pointers), of the
+//   group unions and of work-item counts.
 // k_blocks_fill: ascending column lists from the bitmaps.
-// k_work_fill: work items (a query block and <= chunk key blocks each) and
-//   the split-row table for the combine kernel.
+// k_work_fill: work items (a row group and <= chunk union entries each) and
+//   the split-group table for the combine kernel.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -25,13 +28,16 @@ __global__ __launch_bounds__(256) void k_kminpos(const HeadDev* heads) {
   const HeadDev hd = heads[blockIdx.x];
   const int j = blockIdx.y * 256 + threadIdx.x;
   if (!hd.kminpos || j >= hd.nbk) return;
-  int mn = INT_BIG;
+  int mn = INT_BIG, mx = -1;
+  bool pad = false;
   for (int x = 0; x < B; ++x) {
     const int slot = j * B + x;
     const int p = hd.kperm ? hd.kperm[slot] : (slot < hd.S ? slot : -1);
-    if (p >= 0) mn = min(mn, p);
+    if (p >= 0) { mn = min(mn, p); mx = max(mx, p); }
+    else pad = true;
   }
   hd.kminpos[j] = mn;
+  if (hd.kmaxpos) hd.kmaxpos[j] = pad ? INT_BIG : mx;
 }
 
 __global__ __launch_bounds__(256) void k_minsel_init(OpDev* ops) {
@@ -142,8 +148,7 @@ __device__ void grid_rules(uint32_t* bm, const OpDev& op, int sig, int ph, int L
   __syncthreads();
 }
 
-__global__ __launch_bounds__(256) void k_blocks_count(const HeadDev* heads, const OpDev* ops, Groups g,
-                                                      int chunk) {
+__global__ __launch_bounds__(256) void k_blocks_count(const HeadDev* heads, const OpDev* ops, Groups g) {
   const HeadDev hd = heads[blockIdx.x];
   const int qb = blockIdx.y;
   if (qb >= hd.nbq) return;
@@ -231,18 +236,43 @@ __global__ __launch_bounds__(256) void k_blocks_count(const HeadDev* heads, cons
   }
   atomicAdd(&sh_count, cnt);
   __syncthreads();
-  if (tid == 0) {
-    hd.counts[qb] = sh_count;
-    hd.chunks[qb] = (sh_count + chunk - 1) / chunk;
+  if (tid == 0) hd.counts[qb] = sh_count;
+}
+
+hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* ops, Groups g, int max_nbq,
+                               hipStream_t st) {
+  if (nheads <= 0 || max_nbq <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_blocks_count, dim3(nheads, max_nbq), dim3(256), 0, st, heads, ops, g);
+  return hipGetLastError();
+}
+
+// Size of the union of the key-block sets of the R query blocks of a group.
+__global__ __launch_bounds__(256) void k_group_count(const HeadDev* heads, int R, int chunk) {
+  const HeadDev hd = heads[blockIdx.x];
+  const int gr = blockIdx.y;
+  if (gr >= hd.ngroups) return;
+  __shared__ int sh_count;
+  if (threadIdx.x == 0) sh_count = 0;
+  __syncthreads();
+  const int r0 = gr * R, r1 = min(r0 + R, hd.nbq);
+  int cnt = 0;
+  for (int w = threadIdx.x; w < hd.nwords; w += blockDim.x) {
+    uint32_t u = 0;
+    for (int r = r0; r < r1; ++r) u |= hd.bitmap[(int64_t)r * hd.nwords + w];
+    cnt += __popc(u);
+  }
+  atomicAdd(&sh_count, cnt);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    hd.gcount[gr] = sh_count;
+    hd.chunks[gr] = (sh_count + chunk - 1) / chunk;
   }
 }
 
-hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* ops, Groups g,
-                               const int32_t* tpos, const Segment* segs, int nseg, int max_nbq, int chunk,
-                               hipStream_t st) {
-  (void)tpos; (void)segs; (void)nseg;
-  if (nheads <= 0 || max_nbq <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_blocks_count, dim3(nheads, max_nbq), dim3(256), 0, st, heads, ops, g, chunk);
+hipError_t launch_group_count(const HeadDev* heads, int nheads, int R, int max_groups, int chunk,
+                              hipStream_t st) {
+  if (nheads <= 0 || max_groups <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_group_count, dim3(nheads, max_groups), dim3(256), 0, st, heads, R, chunk);
   return hipGetLastError();
 }
 
@@ -269,11 +299,20 @@ __device__ int block_exscan(int v, int* buf, int& excl) {
 __global__ __launch_bounds__(SCAN_T) void k_blocks_scan(const HeadDev* heads, int64_t* totals) {
   const HeadDev hd = heads[blockIdx.x];
   __shared__ int buf[SCAN_T];
-  int c_nnz = 0, c_items = 0, c_split = 0, c_parts = 0;
+  int c_nnz = 0;
   for (int start = 0; start < hd.nbq; start += SCAN_T) {
     const int i = start + threadIdx.x;
     const int cnt = i < hd.nbq ? hd.counts[i] : 0;
-    const int ch = i < hd.nbq ? hd.chunks[i] : 0;
+    int e0;
+    const int t0 = block_exscan(cnt, buf, e0);
+    if (i < hd.nbq) hd.rowptr[i] = c_nnz + e0;
+    c_nnz += t0;
+  }
+  int c_g = 0, c_items = 0, c_split = 0, c_parts = 0;
+  for (int start = 0; start < hd.ngroups; start += SCAN_T) {
+    const int i = start + threadIdx.x;
+    const int cnt = i < hd.ngroups ? hd.gcount[i] : 0;
+    const int ch = i < hd.ngroups ? hd.chunks[i] : 0;
     const int sp = ch > 1 ? 1 : 0;
     const int pt = ch > 1 ? ch : 0;
     int e0, e1, e2, e3;
@@ -281,20 +320,19 @@ __global__ __launch_bounds__(SCAN_T) void k_blocks_scan(const HeadDev* heads, in
     const int t1 = block_exscan(ch, buf, e1);
     const int t2 = block_exscan(sp, buf, e2);
     const int t3 = block_exscan(pt, buf, e3);
-    if (i < hd.nbq) {
-      hd.rowptr[i] = c_nnz + e0;
+    if (i < hd.ngroups) {
+      hd.growptr[i] = c_g + e0;
       hd.itembase[i] = c_items + e1;
       hd.splitoff[i] = c_split + e2;
       hd.partoff[i] = c_parts + e3;
     }
-    c_nnz += t0; c_items += t1; c_split += t2; c_parts += t3;
+    c_g += t0; c_items += t1; c_split += t2; c_parts += t3;
   }
   if (threadIdx.x == 0) {
     hd.rowptr[hd.nbq] = c_nnz;
-    totals[blockIdx.x * 4 + 0] = c_nnz;
-    totals[blockIdx.x * 4 + 1] = c_items;
-    totals[blockIdx.x * 4 + 2] = c_split;
-    totals[blockIdx.x * 4 + 3] = c_parts;
+    hd.growptr[hd.ngroups] = c_g;
+    int64_t* t = totals + (int64_t)blockIdx.x * NTOT;
+    t[0] = c_nnz; t[1] = c_g; t[2] = c_items; t[3] = c_split; t[4] = c_parts;
   }
 }
 
@@ -333,9 +371,53 @@ __global__ __launch_bounds__(256) void k_blocks_fill(const HeadDev* heads) {
   }
 }
 
-hipError_t launch_blocks_fill(const HeadDev* heads, int nheads, int max_nbq, hipStream_t st) {
+// Union entries of a row group: key block | (bit r set if query block r of
+// the group selects it) << 16, ascending in the key block.
+__global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R) {
+  const HeadDev hd = heads[blockIdx.x];
+  const int gr = blockIdx.y;
+  if (gr >= hd.ngroups) return;
+  __shared__ int buf[256];
+  const int r0 = gr * R, r1 = min(r0 + R, hd.nbq);
+  const int per = (hd.nwords + 255) / 256;
+  const int w0 = threadIdx.x * per;
+  int cnt = 0;
+  for (int w = w0; w < min(w0 + per, hd.nwords); ++w) {
+    uint32_t u = 0;
+    for (int r = r0; r < r1; ++r) u |= hd.bitmap[(int64_t)r * hd.nwords + w];
+    cnt += __popc(u);
+  }
+  buf[threadIdx.x] = cnt;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int t = threadIdx.x >= off ? buf[threadIdx.x - off] : 0;
+    __syncthreads();
+    buf[threadIdx.x] += t;
+    __syncthreads();
+  }
+  int pos = hd.growptr[gr] + buf[threadIdx.x] - cnt;
+  for (int w = w0; w < min(w0 + per, hd.nwords); ++w) {
+    uint32_t rows[4] = {0, 0, 0, 0};
+    uint32_t u = 0;
+    for (int r = r0; r < r1; ++r) {
+      rows[r - r0] = hd.bitmap[(int64_t)r * hd.nwords + w];
+      u |= rows[r - r0];
+    }
+    while (u) {
+      const int b = __ffs(u) - 1;
+      int flags = 0;
+      for (int r = 0; r < r1 - r0; ++r) flags |= ((rows[r] >> b) & 1u) << r;
+      hd.gcol[pos++] = (w * 32 + b) | (flags << 16);
+      u &= u - 1;
+    }
+  }
+}
+
+hipError_t launch_blocks_fill(const HeadDev* heads, int nheads, int max_nbq, int R, int max_groups,
+                              hipStream_t st) {
   if (nheads <= 0 || max_nbq <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_blocks_fill, dim3(nheads, max_nbq), dim3(256), 0, st, heads);
+  hipLaunchKernelGGL(k_group_fill, dim3(nheads, max_groups), dim3(256), 0, st, heads, R);
   return hipGetLastError();
 }
 
@@ -344,17 +426,17 @@ __global__ __launch_bounds__(256) void k_work_fill(const HeadDev* heads, const i
                                                    int chunk, WorkItem* items, SplitRow* splits) {
   const int h = blockIdx.x;
   const HeadDev hd = heads[h];
-  const int qb = blockIdx.y * 256 + threadIdx.x;
-  if (qb >= hd.nbq) return;
-  const int nch = hd.chunks[qb];
-  const int r0 = hd.rowptr[qb], r1 = hd.rowptr[qb + 1];
-  const int64_t ib = item_base[h] + hd.itembase[qb];
+  const int gr = blockIdx.y * 256 + threadIdx.x;
+  if (gr >= hd.ngroups) return;
+  const int nch = hd.chunks[gr];
+  const int r0 = hd.growptr[gr], r1 = hd.growptr[gr + 1];
+  const int64_t ib = item_base[h] + hd.itembase[gr];
   const bool split = nch > 1;
-  const int64_t pb = part_base[h] + hd.partoff[qb];
+  const int64_t pb = part_base[h] + hd.partoff[gr];
   for (int c = 0; c < nch; ++c) {
     WorkItem w;
     w.head = h;
-    w.qblk = qb;
+    w.group = gr;
     w.e0 = r0 + c * chunk;
     w.e1 = min(r0 + (c + 1) * chunk, r1);
     w.part = split ? (int)(pb + c) : -1;
@@ -364,18 +446,18 @@ __global__ __launch_bounds__(256) void k_work_fill(const HeadDev* heads, const i
   if (split) {
     SplitRow s;
     s.head = h;
-    s.qblk = qb;
+    s.group = gr;
     s.part0 = (int)pb;
     s.nparts = nch;
-    splits[split_base[h] + hd.splitoff[qb]] = s;
+    splits[split_base[h] + hd.splitoff[gr]] = s;
   }
 }
 
 hipError_t launch_work_fill(const HeadDev* heads, int nheads, const int64_t* item_base,
-                            const int64_t* part_base, const int64_t* split_base, int max_nbq, int chunk,
+                            const int64_t* part_base, const int64_t* split_base, int max_groups, int chunk,
                             WorkItem* items, SplitRow* splits, hipStream_t st) {
-  if (nheads <= 0 || max_nbq <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_work_fill, dim3(nheads, (max_nbq + 255) / 256), dim3(256), 0, st, heads, item_base,
+  if (nheads <= 0 || max_groups <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_work_fill, dim3(nheads, (max_groups + 255) / 256), dim3(256), 0, st, heads, item_base,
                      part_base, split_base, chunk, items, splits);
   return hipGetLastError();
 }

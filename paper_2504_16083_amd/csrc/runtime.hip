@@ -100,6 +100,7 @@ class Allocator {
 struct mmi_ctx {
   int device = 0;
   int chunk_blocks = 128;
+  int row_group = 4;               // query blocks per attention work item (1, 2 or 4)
   int live_plans = 0;              // plans created from this context and not destroyed
   mmi::Allocator alloc;
   int64_t* pinned = nullptr;       // host staging for totals
@@ -133,7 +134,7 @@ struct HostHead {
   int op0 = 0, nops = 0;
   std::vector<int> op_slot;      // op index -> export slot
   std::vector<EstInfo> est;      // per op
-  int64_t nnz = 0, nitems = 0, nsplit = 0, nparts = 0;
+  int64_t nnz = 0, gnnz = 0, nitems = 0, nsplit = 0, nparts = 0;
 };
 
 }  // namespace mmi
@@ -155,6 +156,7 @@ struct mmi_plan {
   float* d_part_o = nullptr;
   float* d_part_ml = nullptr;
   int64_t nitems = 0, nsplit = 0, nparts = 0;
+  int R = 1;                      // query blocks per attention work item
   int32_t* d_tpos = nullptr;
   std::vector<float*> est_lse2;  // per rowset
   std::vector<std::vector<uint8_t>> keep;   // host sources of asynchronous uploads
@@ -450,7 +452,9 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   for (int gi = 0; gi < g.n; ++gi) nb_groups += (g.len[gi] + B - 1) / B;
 
   P->hh.resize(p.Hq);
-  int max_slots = 0, max_nbq = 0, max_nbk = 0;
+  int max_slots = 0, max_nbq = 0, max_nbk = 0, max_groups = 0;
+  const int R = ctx->row_group;
+  P->R = R;
   for (int h = 0; h < p.Hq; ++h) {
     const mmi_head_cfg& c = cfgs[h];
     HostHead& H = P->hh[h];
@@ -493,6 +497,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
         hd.qperm = dalloc<int32_t>(P, (size_t)nb_all * B);
         hd.kperm = hd.qperm;
         hd.kminpos = dalloc<int32_t>(P, nb_all);
+        hd.kmaxpos = dalloc<int32_t>(P, nb_all);
       }
       P->ops.push_back(d);
       H.est.push_back(e);
@@ -526,6 +531,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
       hd.qperm = dalloc<int32_t>(P, (size_t)nb_groups * B);
       hd.kperm = hd.qperm;
       hd.kminpos = dalloc<int32_t>(P, nb_groups);
+      hd.kmaxpos = dalloc<int32_t>(P, nb_groups);
       const int n0 = (int)P->ops.size();
       P->ops.resize(n0 + g.n * g.n);
       H.est.resize(g.n * g.n);
@@ -591,14 +597,18 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
     H.nops = (int)P->ops.size() - H.op0;
     hd.nwords = (hd.nbk + 31) / 32;
     hd.counts = dalloc<int32_t>(P, hd.nbq);
-    hd.chunks = dalloc<int32_t>(P, hd.nbq);
-    hd.itembase = dalloc<int32_t>(P, hd.nbq);
-    hd.splitoff = dalloc<int32_t>(P, hd.nbq);
-    hd.partoff = dalloc<int32_t>(P, hd.nbq);
     hd.rowptr = dalloc<int32_t>(P, hd.nbq + 1);
     hd.bitmap = dalloc<uint32_t>(P, (size_t)hd.nbq * hd.nwords);
+    hd.ngroups = (hd.nbq + R - 1) / R;
+    hd.gcount = dalloc<int32_t>(P, hd.ngroups);
+    hd.growptr = dalloc<int32_t>(P, hd.ngroups + 1);
+    hd.chunks = dalloc<int32_t>(P, hd.ngroups);
+    hd.itembase = dalloc<int32_t>(P, hd.ngroups);
+    hd.splitoff = dalloc<int32_t>(P, hd.ngroups);
+    hd.partoff = dalloc<int32_t>(P, hd.ngroups);
     max_slots = std::max(max_slots, hd.nbq * B);
     max_nbq = std::max(max_nbq, hd.nbq);
+    max_groups = std::max(max_groups, hd.ngroups);
     max_nbk = std::max(max_nbk, hd.nbk);
     P->heads.push_back(hd);
   }
@@ -625,28 +635,32 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   HIPCHK(launch_perms(P->d_heads, p.Hq, P->d_ops, g, bd.d_tpos, S, max_slots, st));
   HIPCHK(launch_key_summaries(P->d_heads, p.Hq, P->d_ops, (int)P->ops.size(), g, max_nbk, bd.max_sel, st));
   const int chunk = ctx->chunk_blocks;
-  HIPCHK(launch_blocks_count(P->d_heads, p.Hq, P->d_ops, g, bd.d_tpos, d_segs, (int)L.segs.size(), max_nbq,
-                             chunk, st));
-  int64_t* d_tot = dalloc<int64_t>(P, (size_t)p.Hq * 4);
+  HIPCHK(launch_blocks_count(P->d_heads, p.Hq, P->d_ops, g, max_nbq, st));
+  HIPCHK(launch_group_count(P->d_heads, p.Hq, R, max_groups, chunk, st));
+  const size_t ntot = (size_t)p.Hq * NTOT;
+  int64_t* d_tot = dalloc<int64_t>(P, ntot);
   HIPCHK(launch_blocks_scan(P->d_heads, p.Hq, d_tot, st));
-  if (ctx->pinned_n < (size_t)p.Hq * 4) {
+  if (ctx->pinned_n < ntot) {
     if (ctx->pinned) HIPCHK(hipHostFree(ctx->pinned));
     ctx->pinned = nullptr;
-    HIPCHK(hipHostMalloc((void**)&ctx->pinned, sizeof(int64_t) * p.Hq * 4));
-    ctx->pinned_n = (size_t)p.Hq * 4;
+    HIPCHK(hipHostMalloc((void**)&ctx->pinned, sizeof(int64_t) * ntot));
+    ctx->pinned_n = ntot;
   }
-  HIPCHK(hipMemcpyAsync(ctx->pinned, d_tot, sizeof(int64_t) * p.Hq * 4, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipMemcpyAsync(ctx->pinned, d_tot, sizeof(int64_t) * ntot, hipMemcpyDeviceToHost, st));
   HIPCHK(hipStreamSynchronize(st));
 
-  // sizes known: column pool, work items, partials
+  // sizes known: column pools, work items, partials
   std::vector<int64_t> item_base(p.Hq), part_base(p.Hq), split_base(p.Hq);
-  int64_t nnz_all = 0;
+  int64_t nnz_all = 0, gnnz_all = 0;
   for (int h = 0; h < p.Hq; ++h) {
     HostHead& H = P->hh[h];
-    H.nnz = ctx->pinned[h * 4 + 0];
-    H.nitems = ctx->pinned[h * 4 + 1];
-    H.nsplit = ctx->pinned[h * 4 + 2];
-    H.nparts = ctx->pinned[h * 4 + 3];
+    const int64_t* t = ctx->pinned + (size_t)h * NTOT;
+    H.nnz = t[0];
+    H.gnnz = t[1];
+    H.nitems = t[2];
+    H.nsplit = t[3];
+    H.nparts = t[4];
+    gnnz_all += H.gnnz;
     item_base[h] = P->nitems;
     part_base[h] = P->nparts;
     split_base[h] = P->nsplit;
@@ -658,23 +672,26 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   if (P->nitems > 0x7fffffff || P->nparts > 0x7fffffff)
     fail(MMI_ERR_UNSUPPORTED, "work list too large (%lld items)", (long long)P->nitems);
   int32_t* col = dalloc<int32_t>(P, nnz_all);
-  int64_t off = 0;
+  int32_t* gcol = dalloc<int32_t>(P, gnnz_all);
+  int64_t off = 0, goff = 0;
   for (int h = 0; h < p.Hq; ++h) {
     P->heads[h].col = col + off;
+    P->heads[h].gcol = gcol + goff;
     off += P->hh[h].nnz;
+    goff += P->hh[h].gnnz;
   }
   P->keep.emplace_back(reinterpret_cast<const uint8_t*>(P->heads.data()),
                        reinterpret_cast<const uint8_t*>(P->heads.data()) + sizeof(HeadDev) * p.Hq);
   HIPCHK(hipMemcpyAsync(P->d_heads, P->keep.back().data(), sizeof(HeadDev) * p.Hq, hipMemcpyHostToDevice, st));
-  HIPCHK(launch_blocks_fill(P->d_heads, p.Hq, max_nbq, st));
+  HIPCHK(launch_blocks_fill(P->d_heads, p.Hq, max_nbq, R, max_groups, st));
   P->d_items = dalloc<WorkItem>(P, P->nitems);
   P->d_splits = dalloc<SplitRow>(P, P->nsplit);
-  P->d_part_o = dalloc<float>(P, (size_t)std::max<int64_t>(P->nparts, 1) * B * D);
-  P->d_part_ml = dalloc<float>(P, (size_t)std::max<int64_t>(P->nparts, 1) * B * 2);
+  P->d_part_o = dalloc<float>(P, (size_t)std::max<int64_t>(P->nparts, 1) * B * R * D);
+  P->d_part_ml = dalloc<float>(P, (size_t)std::max<int64_t>(P->nparts, 1) * B * R * 2);
   int64_t* d_ib = upload(P, item_base);
   int64_t* d_pb = upload(P, part_base);
   int64_t* d_sb = upload(P, split_base);
-  HIPCHK(launch_work_fill(P->d_heads, p.Hq, d_ib, d_pb, d_sb, max_nbq, chunk, P->d_items, P->d_splits, st));
+  HIPCHK(launch_work_fill(P->d_heads, p.Hq, d_ib, d_pb, d_sb, max_groups, chunk, P->d_items, P->d_splits, st));
   HIPCHK(hipEventRecord(P->ev[3], st));
   P->nnz_all = nnz_all;
 }
@@ -698,6 +715,7 @@ static void plan_execute_impl(mmi_plan* P, const void* q, const void* k, const v
   a.nitems = P->nitems;
   a.part_o = P->d_part_o;
   a.part_ml = P->d_part_ml;
+  a.R = P->R;
   HIPCHK(hipEventRecord(P->ev[4], st));
   HIPCHK(launch_attention(a, st));
   HIPCHK(hipEventRecord(P->ev[5], st));
@@ -764,6 +782,10 @@ int mmi_ctx_create(int device, mmi_ctx** out) {
     if (const char* e = getenv("MMI_CHUNK_BLOCKS")) {
       const int v = atoi(e);
       if (v >= 1) c->chunk_blocks = v;
+    }
+    if (const char* e = getenv("MMI_ROW_GROUP")) {
+      const int v = atoi(e);
+      if (v == 1 || v == 2 || v == 4) c->row_group = v;
     }
     *out = c;
   });

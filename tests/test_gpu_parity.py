@@ -119,3 +119,26 @@ def test_permute_roundtrip(ctx):
     assert torch.equal(y[:S], x[perm[:S].long()])
     assert torch.count_nonzero(y[S:]) == 0
     assert torch.equal(z, x)
+
+
+@pytest.mark.parametrize("R", [1, 2, 4])
+def test_row_group_variants(R, monkeypatch):
+    """Every work-item shape (R query blocks per workgroup) against the oracle,
+    with a small split chunk so long rows are merged by the combine kernel."""
+    say(f"[gpu] row group R={R}")
+    from paper_2504_16083_amd import mmi
+    monkeypatch.setenv("MMI_ROW_GROUP", str(R))
+    monkeypatch.setenv("MMI_CHUNK_BLOCKS", "5")
+    c = mmi.Ctx(0)
+    try:
+        S = 3000
+        mod = _mm_layout(S, 5)
+        q, k, v = _rand_qkv(S, 4, 2, seed=13, scale_k=2.0)
+        heads = [C.global_head(C.dense()), C.global_head(C.grid(20, 40)),
+                 C.qboundary_head({0: C.ashape(32, 200), 1: C.vslash(30, 20)}),
+                 C.boundary2d_head({0: C.ashape(32, 200), 1: C.grid(20, 40)},
+                                   {(0, 1): C.vert(40), (1, 0): C.dense()})]
+        rep = full_check(c, S, 4, 2, mod, heads, q, k, v)
+        say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
+    finally:
+        c.close()
