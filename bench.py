@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8)
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="run one plain copy of this many MiB (k_permute, identity) before the steps, "
+                         "as the reference dispatch for HBM byte counters")
     return ap.parse_args()
 
 
@@ -114,6 +117,15 @@ def main():
     ctx = mmi.Ctx(0)
     prob = mmi.Problem(wl.S, wl.Hq, wl.Hkv, wl.modality)
     stream = torch.cuda.current_stream()
+    if args.calib_copy_mib > 0:
+        rows = args.calib_copy_mib * 1024 * 1024 // 256
+        src = torch.empty(rows, 128, device="cuda", dtype=torch.bfloat16).fill_(1.0)
+        dst = torch.empty_like(src)
+        ident = torch.arange(rows, device="cuda", dtype=torch.int32)
+        mmi.mmi_permute_rows(src, dst, ident, stream)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {rows * 256} bytes read and written")
+        del src, dst, ident
 
     def step():
         plan = mmi.Plan(ctx, prob, wl.heads, q, k, stream)

@@ -75,7 +75,7 @@ class OpState:
     cos: object = None       # grid: coordinate of slot (local slot space)
     g0: object = None        # grid: group start slot per phase
     L: int = 0               # extent of the coordinate system
-    minc: object = None      # grid: smallest coordinate per key block (cache)
+    minc: object = None      # smallest coordinate / admitted position per key block (cache)
 
 
 @dataclass
@@ -343,6 +343,23 @@ def _qb_row(hp: HeadPlan, i: int):
     return np.array(sorted(bs), dtype=np.int64)
 
 
+def _cross_block_min(st: OpState, arrk):
+    """Per key block of the key group: smallest position of a key the cross op
+    admits (every key for dense, the selected columns for VERT). Cached."""
+    if st.minc is None:
+        big = np.iinfo(np.int64).max
+        keys = pad_to_block(arrk.copy())
+        if st.kind == C.OP_DENSE:
+            cand = np.where(keys >= 0, keys, big)
+        elif st.kind == C.OP_VERT:
+            selpos = np.sort(arrk)[st.vsel]
+            cand = np.where((keys >= 0) & np.isin(keys, selpos), keys, big)
+        else:
+            raise ValueError(st.kind)
+        st.minc = cand.reshape(-1, B).min(axis=1)
+    return st.minc
+
+
 def _2d_row(hp: HeadPlan, i: int):
     mq, offq, arrq = _group_of_block(hp, i)
     il = i - offq // B
@@ -363,16 +380,7 @@ def _2d_row(hp: HeadPlan, i: int):
         st = hp.ops[("x", mq, mk)]
         if st.kind == C.OP_NONE:
             continue
-        big = np.iinfo(np.int64).max
-        keys = pad_to_block(arrk.copy())
-        if st.kind == C.OP_DENSE:
-            cand = np.where(keys >= 0, keys, big)
-        elif st.kind == C.OP_VERT:
-            selpos = np.sort(arrk)[st.vsel]
-            cand = np.where((keys >= 0) & np.isin(keys, selpos), keys, big)
-        else:
-            raise ValueError(st.kind)
-        kmin = cand.reshape(-1, B).min(axis=1)
+        kmin = _cross_block_min(st, arrk)
         out.update((kbase + np.nonzero(kmin <= maxpos)[0]).tolist())
     return np.array(sorted(out), dtype=np.int64)
 

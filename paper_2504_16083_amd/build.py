@@ -38,7 +38,7 @@ def build(verbose: bool = False) -> str:
             if verbose and msg:
                 print(msg, file=sys.stderr)
     tmp = LIB + ".tmp"
-    _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *objs])
+    _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-Wl,--no-undefined", "-o", tmp, *objs])
     os.replace(tmp, LIB)
     return LIB
 

@@ -102,6 +102,7 @@ struct HeadDev {
   int32_t* gcount;            // [ngroups] union sizes
   int32_t* growptr;           // [ngroups+1]
   int32_t* gcol;              // [gnnz]
+  int32_t* chunklen;          // [1] union entries per work item for this head (set by the scan)
   int32_t* chunks;            // [ngroups] work items per group
   int32_t* itembase;          // [ngroups] exclusive prefix of chunks
   int32_t* splitoff;          // [ngroups] exclusive prefix of (chunks > 1)
@@ -147,16 +148,17 @@ hipError_t launch_key_summaries(const HeadDev* heads, int nheads, OpDev* ops, in
                                 Groups g, int max_nbk, int max_sel, hipStream_t st);
 hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* ops, Groups g, int max_nbq,
                                hipStream_t st);
-hipError_t launch_group_count(const HeadDev* heads, int nheads, int R, int max_groups, int chunk_blocks,
-                              hipStream_t st);
+hipError_t launch_group_count(const HeadDev* heads, int nheads, int R, int max_groups, hipStream_t st);
 // totals[head] = {nnz, gnnz, nitems, nsplit, nparts}
 constexpr int NTOT = 5;
-hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int64_t* totals, hipStream_t st);
+// Work-item length per head: max(min_chunk, ceil(gnnz_head / items_per_head)).
+hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int min_chunk, int items_per_head,
+                              int64_t* totals, hipStream_t st);
 hipError_t launch_blocks_fill(const HeadDev* heads, int nheads, int max_nbq, int R, int max_groups,
                               hipStream_t st);
 hipError_t launch_work_fill(const HeadDev* heads, int nheads, const int64_t* item_base,
                             const int64_t* part_base, const int64_t* split_base, int max_groups,
-                            int chunk_blocks, WorkItem* items, SplitRow* splits, hipStream_t st);
+                            WorkItem* items, SplitRow* splits, hipStream_t st);
 // k_attention.hip
 struct AttnArgs {
   Tensor q, k, v;

@@ -247,7 +247,7 @@ hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* op
 }
 
 // Size of the union of the key-block sets of the R query blocks of a group.
-__global__ __launch_bounds__(256) void k_group_count(const HeadDev* heads, int R, int chunk) {
+__global__ __launch_bounds__(256) void k_group_count(const HeadDev* heads, int R) {
   const HeadDev hd = heads[blockIdx.x];
   const int gr = blockIdx.y;
   if (gr >= hd.ngroups) return;
@@ -263,16 +263,12 @@ __global__ __launch_bounds__(256) void k_group_count(const HeadDev* heads, int R
   }
   atomicAdd(&sh_count, cnt);
   __syncthreads();
-  if (threadIdx.x == 0) {
-    hd.gcount[gr] = sh_count;
-    hd.chunks[gr] = (sh_count + chunk - 1) / chunk;
-  }
+  if (threadIdx.x == 0) hd.gcount[gr] = sh_count;
 }
 
-hipError_t launch_group_count(const HeadDev* heads, int nheads, int R, int max_groups, int chunk,
-                              hipStream_t st) {
+hipError_t launch_group_count(const HeadDev* heads, int nheads, int R, int max_groups, hipStream_t st) {
   if (nheads <= 0 || max_groups <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_group_count, dim3(nheads, max_groups), dim3(256), 0, st, heads, R, chunk);
+  hipLaunchKernelGGL(k_group_count, dim3(nheads, max_groups), dim3(256), 0, st, heads, R);
   return hipGetLastError();
 }
 
@@ -296,7 +292,8 @@ __device__ int block_exscan(int v, int* buf, int& excl) {
   return tot;
 }
 
-__global__ __launch_bounds__(SCAN_T) void k_blocks_scan(const HeadDev* heads, int64_t* totals) {
+__global__ __launch_bounds__(SCAN_T) void k_blocks_scan(const HeadDev* heads, int min_chunk, int items_per_head,
+                                                        int64_t* totals) {
   const HeadDev hd = heads[blockIdx.x];
   __shared__ int buf[SCAN_T];
   int c_nnz = 0;
@@ -308,40 +305,53 @@ __global__ __launch_bounds__(SCAN_T) void k_blocks_scan(const HeadDev* heads, in
     if (i < hd.nbq) hd.rowptr[i] = c_nnz + e0;
     c_nnz += t0;
   }
-  int c_g = 0, c_items = 0, c_split = 0, c_parts = 0;
+  int c_g = 0;
   for (int start = 0; start < hd.ngroups; start += SCAN_T) {
     const int i = start + threadIdx.x;
     const int cnt = i < hd.ngroups ? hd.gcount[i] : 0;
-    const int ch = i < hd.ngroups ? hd.chunks[i] : 0;
+    int e0;
+    const int t0 = block_exscan(cnt, buf, e0);
+    if (i < hd.ngroups) hd.growptr[i] = c_g + e0;
+    c_g += t0;
+  }
+  // long unions are split so that no work item holds much more than a
+  // 1/items_per_head share of the head's work
+  const int chunk = max(min_chunk, (int)(((int64_t)c_g + items_per_head - 1) / items_per_head));
+  int c_items = 0, c_split = 0, c_parts = 0;
+  for (int start = 0; start < hd.ngroups; start += SCAN_T) {
+    const int i = start + threadIdx.x;
+    const int ch = i < hd.ngroups ? (hd.gcount[i] + chunk - 1) / chunk : 0;
     const int sp = ch > 1 ? 1 : 0;
     const int pt = ch > 1 ? ch : 0;
-    int e0, e1, e2, e3;
-    const int t0 = block_exscan(cnt, buf, e0);
+    int e1, e2, e3;
     const int t1 = block_exscan(ch, buf, e1);
     const int t2 = block_exscan(sp, buf, e2);
     const int t3 = block_exscan(pt, buf, e3);
     if (i < hd.ngroups) {
-      hd.growptr[i] = c_g + e0;
+      hd.chunks[i] = ch;
       hd.itembase[i] = c_items + e1;
       hd.splitoff[i] = c_split + e2;
       hd.partoff[i] = c_parts + e3;
     }
-    c_g += t0; c_items += t1; c_split += t2; c_parts += t3;
+    c_items += t1; c_split += t2; c_parts += t3;
   }
   if (threadIdx.x == 0) {
     hd.rowptr[hd.nbq] = c_nnz;
     hd.growptr[hd.ngroups] = c_g;
+    hd.chunklen[0] = chunk;
     int64_t* t = totals + (int64_t)blockIdx.x * NTOT;
     t[0] = c_nnz; t[1] = c_g; t[2] = c_items; t[3] = c_split; t[4] = c_parts;
   }
 }
 
-hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int64_t* totals, hipStream_t st) {
+hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int min_chunk, int items_per_head,
+                              int64_t* totals, hipStream_t st) {
   if (nheads <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_blocks_scan, dim3(nheads), dim3(SCAN_T), 0, st, heads, totals);
+  hipLaunchKernelGGL(k_blocks_scan, dim3(nheads), dim3(SCAN_T), 0, st, heads, min_chunk, items_per_head, totals);
   return hipGetLastError();
 }
 
+// Ascending column list of one query block from its bitmap.
 __global__ __launch_bounds__(256) void k_blocks_fill(const HeadDev* heads) {
   const HeadDev hd = heads[blockIdx.x];
   const int qb = blockIdx.y;
@@ -423,11 +433,12 @@ hipError_t launch_blocks_fill(const HeadDev* heads, int nheads, int max_nbq, int
 
 __global__ __launch_bounds__(256) void k_work_fill(const HeadDev* heads, const int64_t* item_base,
                                                    const int64_t* part_base, const int64_t* split_base,
-                                                   int chunk, WorkItem* items, SplitRow* splits) {
+                                                   WorkItem* items, SplitRow* splits) {
   const int h = blockIdx.x;
   const HeadDev hd = heads[h];
   const int gr = blockIdx.y * 256 + threadIdx.x;
   if (gr >= hd.ngroups) return;
+  const int chunk = hd.chunklen[0];
   const int nch = hd.chunks[gr];
   const int r0 = hd.growptr[gr], r1 = hd.growptr[gr + 1];
   const int64_t ib = item_base[h] + hd.itembase[gr];
@@ -454,11 +465,11 @@ __global__ __launch_bounds__(256) void k_work_fill(const HeadDev* heads, const i
 }
 
 hipError_t launch_work_fill(const HeadDev* heads, int nheads, const int64_t* item_base,
-                            const int64_t* part_base, const int64_t* split_base, int max_groups, int chunk,
+                            const int64_t* part_base, const int64_t* split_base, int max_groups,
                             WorkItem* items, SplitRow* splits, hipStream_t st) {
   if (nheads <= 0 || max_groups <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_work_fill, dim3(nheads, (max_groups + 255) / 256), dim3(256), 0, st, heads, item_base,
-                     part_base, split_base, chunk, items, splits);
+                     part_base, split_base, items, splits);
   return hipGetLastError();
 }
 

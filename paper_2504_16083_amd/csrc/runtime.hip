@@ -99,7 +99,8 @@ class Allocator {
 
 struct mmi_ctx {
   int device = 0;
-  int chunk_blocks = 128;
+  int chunk_blocks = 64;           // smallest work-item length (union entries)
+  int items_per_layer = 8192;      // target number of work items per layer
   int row_group = 4;               // query blocks per attention work item (1, 2 or 4)
   int live_plans = 0;              // plans created from this context and not destroyed
   mmi::Allocator alloc;
@@ -602,6 +603,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
     hd.ngroups = (hd.nbq + R - 1) / R;
     hd.gcount = dalloc<int32_t>(P, hd.ngroups);
     hd.growptr = dalloc<int32_t>(P, hd.ngroups + 1);
+    hd.chunklen = dalloc<int32_t>(P, 1);
     hd.chunks = dalloc<int32_t>(P, hd.ngroups);
     hd.itembase = dalloc<int32_t>(P, hd.ngroups);
     hd.splitoff = dalloc<int32_t>(P, hd.ngroups);
@@ -636,10 +638,11 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   HIPCHK(launch_key_summaries(P->d_heads, p.Hq, P->d_ops, (int)P->ops.size(), g, max_nbk, bd.max_sel, st));
   const int chunk = ctx->chunk_blocks;
   HIPCHK(launch_blocks_count(P->d_heads, p.Hq, P->d_ops, g, max_nbq, st));
-  HIPCHK(launch_group_count(P->d_heads, p.Hq, R, max_groups, chunk, st));
+  HIPCHK(launch_group_count(P->d_heads, p.Hq, R, max_groups, st));
   const size_t ntot = (size_t)p.Hq * NTOT;
   int64_t* d_tot = dalloc<int64_t>(P, ntot);
-  HIPCHK(launch_blocks_scan(P->d_heads, p.Hq, d_tot, st));
+  const int items_per_head = std::max(1, ctx->items_per_layer / p.Hq);
+  HIPCHK(launch_blocks_scan(P->d_heads, p.Hq, chunk, items_per_head, d_tot, st));
   if (ctx->pinned_n < ntot) {
     if (ctx->pinned) HIPCHK(hipHostFree(ctx->pinned));
     ctx->pinned = nullptr;
@@ -691,7 +694,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   int64_t* d_ib = upload(P, item_base);
   int64_t* d_pb = upload(P, part_base);
   int64_t* d_sb = upload(P, split_base);
-  HIPCHK(launch_work_fill(P->d_heads, p.Hq, d_ib, d_pb, d_sb, max_groups, chunk, P->d_items, P->d_splits, st));
+  HIPCHK(launch_work_fill(P->d_heads, p.Hq, d_ib, d_pb, d_sb, max_groups, P->d_items, P->d_splits, st));
   HIPCHK(hipEventRecord(P->ev[3], st));
   P->nnz_all = nnz_all;
 }
@@ -782,6 +785,10 @@ int mmi_ctx_create(int device, mmi_ctx** out) {
     if (const char* e = getenv("MMI_CHUNK_BLOCKS")) {
       const int v = atoi(e);
       if (v >= 1) c->chunk_blocks = v;
+    }
+    if (const char* e = getenv("MMI_ITEMS_PER_LAYER")) {
+      const int v = atoi(e);
+      if (v >= 1) c->items_per_layer = v;
     }
     if (const char* e = getenv("MMI_ROW_GROUP")) {
       const int v = atoi(e);
