@@ -118,6 +118,7 @@ typedef struct mmi_head_stats {
   int32_t split_rows;            /* query blocks split across work items */
   int32_t sigma[MMI_MAX_MODALITIES];  /* chosen Grid stride per op slot (0 = not Grid / dense fallback) */
   int32_t phase[MMI_MAX_MODALITIES];
+  int32_t group_stride;          /* query-block stride of the attention row groups (1, 2, 4 or 8) */
 } mmi_head_stats;
 
 /* Stage durations of a plan, from HIP events recorded on the plan's stream

@@ -36,6 +36,15 @@ __device__ __forceinline__ bf16x8 zero8() {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
+// Query block held by member r of row group g (R members, row stride rho).
+__host__ __device__ inline int group_row(int g, int r, int R, int rho) {
+  return (g / rho) * (R * rho) + (g % rho) + r * rho;
+}
+
+__host__ __device__ inline int groups_for(int nbq, int R, int rho) {
+  return (nbq + R * rho - 1) / (R * rho) * rho;
+}
+
 // ------------------------------------------------------------------ Grid geometry
 // Tokens with coordinates [0, L) are grouped by phase (coordinate mod s); the
 // groups are ordered p+1, p+2, ..., p (mod s) and packed without padding.

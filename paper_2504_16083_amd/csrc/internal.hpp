@@ -95,11 +95,13 @@ struct HeadDev {
   int32_t nwords;
   int32_t* col;               // [nnz]
   int32_t op0;                // first OpDev of this head
-  // Row groups: R consecutive query blocks processed by one work item over the
-  // union of their key lists (entries: key block | flags << 16, bit r of the
-  // flags = query block r of the group selects that key block).
-  int32_t ngroups;
-  int32_t* gcount;            // [ngroups] union sizes
+  // Row groups: R query blocks processed by one work item over the union of
+  // their key lists (entries: key block | flags << 16, bit r of the flags =
+  // member r selects that key block). Member r of group g is query block
+  // (g / rho) * R * rho + g % rho + r * rho; rho is chosen per head.
+  int32_t gcap;               // capacity of the per-group arrays (>= groups for any stride)
+  int32_t* gp;                // [2] chosen row stride rho of the groups, number of groups
+  int32_t* gcount;            // [groups] union sizes
   int32_t* growptr;           // [ngroups+1]
   int32_t* gcol;              // [gnnz]
   int32_t* chunklen;          // [1] union entries per work item for this head (set by the scan)
@@ -147,6 +149,10 @@ hipError_t launch_topk(const TopkJob* jobs, int njobs, hipStream_t st);
 hipError_t launch_key_summaries(const HeadDev* heads, int nheads, OpDev* ops, int nops,
                                 Groups g, int max_nbk, int max_sel, hipStream_t st);
 hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* ops, Groups g, int max_nbq,
+                               hipStream_t st);
+// Chooses each head's row stride rho in {1, 2, 4, 8} (smallest total union,
+// ties to the smaller rho); cand: int64 scratch [nheads][4].
+hipError_t launch_group_stride(const HeadDev* heads, int nheads, int R, int max_groups, int64_t* cand,
                                hipStream_t st);
 hipError_t launch_group_count(const HeadDev* heads, int nheads, int R, int max_groups, hipStream_t st);
 // totals[head] = {nnz, gnnz, nitems, nsplit, nparts}

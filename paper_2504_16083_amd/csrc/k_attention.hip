@@ -145,8 +145,8 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(2))) vo
   const HeadDev hd = a.heads[w.head];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int c = lane & 31, h = lane >> 5;
-  const int rb = wave >> 1;                        // query block of the group owned by this wave
-  const int qblk = w.group * R + rb;
+  const int rb = wave >> 1;                        // member of the group owned by this wave
+  const int qblk = group_row(w.group, rb, R, hd.gp[0]);
   const int qpos = qblk < hd.nbq ? slot_pos(hd.qperm, qblk * B + (wave & 1) * 32 + c, a.S) : -1;
   int qmin = qpos >= 0 ? qpos : INT_BIG;      // smallest valid query position of the wave
 #pragma unroll
@@ -289,7 +289,7 @@ __global__ __launch_bounds__(256) void k_combine(AttnArgs a, const SplitRow* spl
   const SplitRow sr = splits[blockIdx.x];
   const HeadDev hd = a.heads[sr.head];
   const int rb = blockIdx.y;
-  const int qblk = sr.group * a.R + rb;
+  const int qblk = group_row(sr.group, rb, a.R, hd.gp[0]);
   if (qblk >= hd.nbq) return;
   const int row = rb * B + (threadIdx.x >> 2), quarter = threadIdx.x & 3;
   const int qpos = slot_pos(hd.qperm, qblk * B + (threadIdx.x >> 2), a.S);

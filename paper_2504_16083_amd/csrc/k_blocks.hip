@@ -246,22 +246,70 @@ hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* op
   return hipGetLastError();
 }
 
-// Size of the union of the key-block sets of the R query blocks of a group.
-__global__ __launch_bounds__(256) void k_group_count(const HeadDev* heads, int R) {
-  const HeadDev hd = heads[blockIdx.x];
-  const int gr = blockIdx.y;
-  if (gr >= hd.ngroups) return;
-  __shared__ int sh_count;
-  if (threadIdx.x == 0) sh_count = 0;
-  __syncthreads();
-  const int r0 = gr * R, r1 = min(r0 + R, hd.nbq);
+// Union size of the key-block sets of a group's members.
+__device__ int union_count(const HeadDev& hd, int g, int R, int rho) {
   int cnt = 0;
   for (int w = threadIdx.x; w < hd.nwords; w += blockDim.x) {
     uint32_t u = 0;
-    for (int r = r0; r < r1; ++r) u |= hd.bitmap[(int64_t)r * hd.nwords + w];
+    for (int r = 0; r < R; ++r) {
+      const int row = group_row(g, r, R, rho);
+      if (row < hd.nbq) u |= hd.bitmap[(int64_t)row * hd.nwords + w];
+    }
     cnt += __popc(u);
   }
-  atomicAdd(&sh_count, cnt);
+  return cnt;
+}
+
+__global__ void k_zero64(int64_t* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+__global__ __launch_bounds__(256) void k_group_eval(const HeadDev* heads, int R, int64_t* cand) {
+  const HeadDev hd = heads[blockIdx.x];
+  const int g = blockIdx.y;
+  __shared__ int sh;
+  for (int c = 0; c < 4; ++c) {
+    const int rho = 1 << c;
+    if (g >= groups_for(hd.nbq, R, rho)) continue;      // uniform over the block
+    if (threadIdx.x == 0) sh = 0;
+    __syncthreads();
+    atomicAdd(&sh, union_count(hd, g, R, rho));
+    __syncthreads();
+    if (threadIdx.x == 0) atomicAdd(reinterpret_cast<unsigned long long*>(&cand[blockIdx.x * 4 + c]),
+                                    (unsigned long long)sh);
+    __syncthreads();
+  }
+}
+
+__global__ void k_group_pick(const HeadDev* heads, int nheads, int R, const int64_t* cand) {
+  const int h = blockIdx.x * blockDim.x + threadIdx.x;
+  if (h >= nheads) return;
+  const HeadDev hd = heads[h];
+  int best = 0;
+  for (int c = 1; c < 4; ++c)
+    if (cand[h * 4 + c] < cand[h * 4 + best]) best = c;
+  hd.gp[0] = 1 << best;
+  hd.gp[1] = groups_for(hd.nbq, R, 1 << best);
+}
+
+hipError_t launch_group_stride(const HeadDev* heads, int nheads, int R, int max_groups, int64_t* cand,
+                               hipStream_t st) {
+  if (nheads <= 0 || max_groups <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_zero64, dim3((nheads * 4 + 255) / 256), dim3(256), 0, st, cand, nheads * 4);
+  hipLaunchKernelGGL(k_group_eval, dim3(nheads, max_groups), dim3(256), 0, st, heads, R, cand);
+  hipLaunchKernelGGL(k_group_pick, dim3((nheads + 63) / 64), dim3(64), 0, st, heads, nheads, R, cand);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void k_group_count(const HeadDev* heads, int R) {
+  const HeadDev hd = heads[blockIdx.x];
+  const int gr = blockIdx.y;
+  if (gr >= hd.gp[1]) return;
+  __shared__ int sh_count;
+  if (threadIdx.x == 0) sh_count = 0;
+  __syncthreads();
+  atomicAdd(&sh_count, union_count(hd, gr, R, hd.gp[0]));
   __syncthreads();
   if (threadIdx.x == 0) hd.gcount[gr] = sh_count;
 }
@@ -305,29 +353,30 @@ __global__ __launch_bounds__(SCAN_T) void k_blocks_scan(const HeadDev* heads, in
     if (i < hd.nbq) hd.rowptr[i] = c_nnz + e0;
     c_nnz += t0;
   }
+  const int ngroups = hd.gp[1];
   int c_g = 0;
-  for (int start = 0; start < hd.ngroups; start += SCAN_T) {
+  for (int start = 0; start < ngroups; start += SCAN_T) {
     const int i = start + threadIdx.x;
-    const int cnt = i < hd.ngroups ? hd.gcount[i] : 0;
+    const int cnt = i < ngroups ? hd.gcount[i] : 0;
     int e0;
     const int t0 = block_exscan(cnt, buf, e0);
-    if (i < hd.ngroups) hd.growptr[i] = c_g + e0;
+    if (i < ngroups) hd.growptr[i] = c_g + e0;
     c_g += t0;
   }
   // long unions are split so that no work item holds much more than a
   // 1/items_per_head share of the head's work
   const int chunk = max(min_chunk, (int)(((int64_t)c_g + items_per_head - 1) / items_per_head));
   int c_items = 0, c_split = 0, c_parts = 0;
-  for (int start = 0; start < hd.ngroups; start += SCAN_T) {
+  for (int start = 0; start < ngroups; start += SCAN_T) {
     const int i = start + threadIdx.x;
-    const int ch = i < hd.ngroups ? (hd.gcount[i] + chunk - 1) / chunk : 0;
+    const int ch = i < ngroups ? (hd.gcount[i] + chunk - 1) / chunk : 0;
     const int sp = ch > 1 ? 1 : 0;
     const int pt = ch > 1 ? ch : 0;
     int e1, e2, e3;
     const int t1 = block_exscan(ch, buf, e1);
     const int t2 = block_exscan(sp, buf, e2);
     const int t3 = block_exscan(pt, buf, e3);
-    if (i < hd.ngroups) {
+    if (i < ngroups) {
       hd.chunks[i] = ch;
       hd.itembase[i] = c_items + e1;
       hd.splitoff[i] = c_split + e2;
@@ -337,7 +386,7 @@ __global__ __launch_bounds__(SCAN_T) void k_blocks_scan(const HeadDev* heads, in
   }
   if (threadIdx.x == 0) {
     hd.rowptr[hd.nbq] = c_nnz;
-    hd.growptr[hd.ngroups] = c_g;
+    hd.growptr[ngroups] = c_g;
     hd.chunklen[0] = chunk;
     int64_t* t = totals + (int64_t)blockIdx.x * NTOT;
     t[0] = c_nnz; t[1] = c_g; t[2] = c_items; t[3] = c_split; t[4] = c_parts;
@@ -386,15 +435,18 @@ __global__ __launch_bounds__(256) void k_blocks_fill(const HeadDev* heads) {
 __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R) {
   const HeadDev hd = heads[blockIdx.x];
   const int gr = blockIdx.y;
-  if (gr >= hd.ngroups) return;
+  if (gr >= hd.gp[1]) return;
+  const int rho = hd.gp[0];
   __shared__ int buf[256];
-  const int r0 = gr * R, r1 = min(r0 + R, hd.nbq);
+  int rows[4];
+  for (int r = 0; r < 4; ++r) rows[r] = r < R ? group_row(gr, r, R, rho) : hd.nbq;
   const int per = (hd.nwords + 255) / 256;
   const int w0 = threadIdx.x * per;
   int cnt = 0;
   for (int w = w0; w < min(w0 + per, hd.nwords); ++w) {
     uint32_t u = 0;
-    for (int r = r0; r < r1; ++r) u |= hd.bitmap[(int64_t)r * hd.nwords + w];
+    for (int r = 0; r < R; ++r)
+      if (rows[r] < hd.nbq) u |= hd.bitmap[(int64_t)rows[r] * hd.nwords + w];
     cnt += __popc(u);
   }
   buf[threadIdx.x] = cnt;
@@ -407,16 +459,16 @@ __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R)
   }
   int pos = hd.growptr[gr] + buf[threadIdx.x] - cnt;
   for (int w = w0; w < min(w0 + per, hd.nwords); ++w) {
-    uint32_t rows[4] = {0, 0, 0, 0};
+    uint32_t bits[4] = {0, 0, 0, 0};
     uint32_t u = 0;
-    for (int r = r0; r < r1; ++r) {
-      rows[r - r0] = hd.bitmap[(int64_t)r * hd.nwords + w];
-      u |= rows[r - r0];
+    for (int r = 0; r < R; ++r) {
+      if (rows[r] < hd.nbq) bits[r] = hd.bitmap[(int64_t)rows[r] * hd.nwords + w];
+      u |= bits[r];
     }
     while (u) {
       const int b = __ffs(u) - 1;
       int flags = 0;
-      for (int r = 0; r < r1 - r0; ++r) flags |= ((rows[r] >> b) & 1u) << r;
+      for (int r = 0; r < R; ++r) flags |= ((bits[r] >> b) & 1u) << r;
       hd.gcol[pos++] = (w * 32 + b) | (flags << 16);
       u &= u - 1;
     }
@@ -437,7 +489,7 @@ __global__ __launch_bounds__(256) void k_work_fill(const HeadDev* heads, const i
   const int h = blockIdx.x;
   const HeadDev hd = heads[h];
   const int gr = blockIdx.y * 256 + threadIdx.x;
-  if (gr >= hd.ngroups) return;
+  if (gr >= hd.gp[1]) return;
   const int chunk = hd.chunklen[0];
   const int nch = hd.chunks[gr];
   const int r0 = hd.growptr[gr], r1 = hd.growptr[gr + 1];

@@ -600,17 +600,18 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
     hd.counts = dalloc<int32_t>(P, hd.nbq);
     hd.rowptr = dalloc<int32_t>(P, hd.nbq + 1);
     hd.bitmap = dalloc<uint32_t>(P, (size_t)hd.nbq * hd.nwords);
-    hd.ngroups = (hd.nbq + R - 1) / R;
-    hd.gcount = dalloc<int32_t>(P, hd.ngroups);
-    hd.growptr = dalloc<int32_t>(P, hd.ngroups + 1);
+    hd.gcap = (hd.nbq + R - 1) / R + 8;       // >= groups_for(nbq, R, rho) for rho <= 8
+    hd.gp = dalloc<int32_t>(P, 2);
+    hd.gcount = dalloc<int32_t>(P, hd.gcap);
+    hd.growptr = dalloc<int32_t>(P, hd.gcap + 1);
     hd.chunklen = dalloc<int32_t>(P, 1);
-    hd.chunks = dalloc<int32_t>(P, hd.ngroups);
-    hd.itembase = dalloc<int32_t>(P, hd.ngroups);
-    hd.splitoff = dalloc<int32_t>(P, hd.ngroups);
-    hd.partoff = dalloc<int32_t>(P, hd.ngroups);
+    hd.chunks = dalloc<int32_t>(P, hd.gcap);
+    hd.itembase = dalloc<int32_t>(P, hd.gcap);
+    hd.splitoff = dalloc<int32_t>(P, hd.gcap);
+    hd.partoff = dalloc<int32_t>(P, hd.gcap);
     max_slots = std::max(max_slots, hd.nbq * B);
     max_nbq = std::max(max_nbq, hd.nbq);
-    max_groups = std::max(max_groups, hd.ngroups);
+    max_groups = std::max(max_groups, hd.gcap);
     max_nbk = std::max(max_nbk, hd.nbk);
     P->heads.push_back(hd);
   }
@@ -638,6 +639,8 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   HIPCHK(launch_key_summaries(P->d_heads, p.Hq, P->d_ops, (int)P->ops.size(), g, max_nbk, bd.max_sel, st));
   const int chunk = ctx->chunk_blocks;
   HIPCHK(launch_blocks_count(P->d_heads, p.Hq, P->d_ops, g, max_nbq, st));
+  int64_t* d_cand = dalloc<int64_t>(P, (size_t)p.Hq * 4);
+  HIPCHK(launch_group_stride(P->d_heads, p.Hq, R, max_groups, d_cand, st));
   HIPCHK(launch_group_count(P->d_heads, p.Hq, R, max_groups, st));
   const size_t ntot = (size_t)p.Hq * NTOT;
   int64_t* d_tot = dalloc<int64_t>(P, ntot);
@@ -880,6 +883,9 @@ int mmi_plan_stats(mmi_plan* P, int head, mmi_head_stats* out) {
         if (slot < MMI_MAX_MODALITIES) { s.sigma[slot] = prm[0]; s.phase[slot] = prm[1]; }
       }
     }
+    int32_t gp[2];
+    HIPCHK(hipMemcpy(gp, hd.gp, sizeof gp, hipMemcpyDeviceToHost));
+    s.group_stride = gp[0];
     *out = s;
   });
 }

@@ -170,3 +170,62 @@ def full_check(ctx, S, Hq, Hkv, modality, heads, q, k, v, rows=None, heads_to_ch
     finally:
         plan.destroy()
     return rep
+
+
+def sample_rows(S, modality, rng, n_uniform=64, last=64, around=8):
+    """Stratified query rows: the last rows, rows on both sides of every
+    modality boundary, and uniform rows (seeded)."""
+    rows = set(range(max(0, S - last), S))
+    if modality is not None:
+        cut = np.nonzero(np.diff(np.asarray(modality).astype(np.int16)))[0] + 1
+        for c in cut[:64]:
+            rows.update(range(max(0, c - around), min(S, c + around)))
+    rows.update(rng.choice(S, size=min(n_uniform, S), replace=False).tolist())
+    return np.array(sorted(rows), dtype=np.int64)
+
+
+def sampled_check(ctx, wl, q, k, v, heads_to_check, rows_extra=None, seed=0):
+    """Full-size parity: every head's scores, choices, permutations and block
+    index are compared in full; O/LSE on stratified sampled rows (including
+    each Grid head's first horizontal-line rows)."""
+    plan, o, lse = run_gpu(ctx, wl.S, wl.Hq, wl.Hkv, wl.modality, wl.heads, q, k, v)
+    G = wl.Hq // wl.Hkv
+    rng = np.random.default_rng(seed)
+    base_rows = sample_rows(wl.S, wl.modality, rng)
+    kv_cache = {}
+
+    def kv(g):
+        if g not in kv_cache:
+            kv_cache.clear()
+            kv_cache[g] = (ON.torch_bf16_to_f64(k[:, g]), ON.torch_bf16_to_f64(v[:, g]))
+        return kv_cache[g]
+
+    rep = Report()
+    try:
+        for h in heads_to_check:
+            qh = q[:, h]
+
+            def q_rows(r, qh=qh):
+                return ON.torch_bf16_to_f64(qh[torch.as_tensor(np.asarray(r), device=qh.device)])
+
+            K, V = kv(h // G)
+            hp = OP.plan_head(wl.heads[h], wl.S, wl.modality, q_rows, K)
+            if not compare_head(plan, h, hp, rep):
+                continue
+            rows = base_rows
+            if hp.qperm is not None and hp.nbq:
+                lastblk = hp.qperm[(hp.nbq - 1) * OP.B:hp.nbq * OP.B]
+                rows = np.union1d(rows, lastblk[lastblk >= 0][:8])
+            Oo, Lo = OA.head_rows(hp, q_rows, K, V, rows)
+            Og = ON.torch_bf16_to_f64(o[torch.as_tensor(rows, device=o.device), h])
+            Lg = lse[h, torch.as_tensor(rows, device=lse.device)].cpu().double().numpy()
+            eo = float(np.abs(Og - Oo).max())
+            el = float((np.abs(Lg - Lo) / np.maximum(1.0, np.abs(Lo))).max())
+            rep.max_o = max(rep.max_o, eo)
+            rep.max_lse = max(rep.max_lse, el)
+            rep.rows += len(rows)
+            assert eo <= O_TOL, f"head {h}: max |O - O_oracle| = {eo}"
+            assert el <= LSE_TOL, f"head {h}: LSE rel err {el}"
+    finally:
+        plan.destroy()
+    return rep

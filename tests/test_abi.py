@@ -80,3 +80,9 @@ def test_ctx_without_device_is_an_error():
         mmi.lib().mmi_ctx_destroy(h)
     else:
         assert rc in (-1, -5) and mmi.mmi_last_error()
+
+
+def test_stats_struct_matches_header():
+    # kind, n_qblocks, n_kblocks (12) + pad (4) + 2 x int64 (16) + split_rows (4) + 2 x 8 int32 (64)
+    assert mmi.mmi_head_stats.group_stride.offset == 100
+    assert ct.sizeof(mmi.mmi_head_stats) == 104
