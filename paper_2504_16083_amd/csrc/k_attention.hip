@@ -4,39 +4,38 @@
 // qperm / kperm say which token each slot holds, the block index says which
 // key blocks each query block visits).
 //
-// One work item = a row group of R consecutive permuted query blocks and a
-// contiguous range of the union of their key-block lists; each union entry
-// carries one flag per query block. The workgroup has 2R waves; waves 2r and
-// 2r+1 own the 64 rows of query block r (32 rows each). Every key block of
-// the range is loaded from HBM/L2 once into LDS and used by all query blocks
-// that selected it, so each byte of K/V feeds up to 64R rows. Per key block
-// and active wave:
+// One work item = a row group of R permuted query blocks and a contiguous
+// range of the union of their key-block lists; each union entry carries one
+// flag per query block. The workgroup has 2R waves; waves 2r and 2r+1 own
+// the 64 rows of member r (32 rows each). Every key block of the range is
+// loaded once into LDS and used by all members that selected it. Per key
+// block and active wave:
 //   S^T (64 keys x 32 queries) = K Q^T         16 MFMA 32x32x16 bf16
 //   mask by original positions (k <= q) where the block reaches past the
 //   wave's first query, online softmax in fp32 (log2 domain)
 //   O^T (128 x 32) += V^T P^T                  16 MFMA 32x32x16 bf16
-// Computing S^T rather than S puts one query per lane, so the row max/sum
-// needs one cross-lane exchange and the accumulator doubles as the P operand
-// of the PV product (the key order inside the contraction is permuted the
-// same way in V^T). K is staged row-major and V transposed in LDS; the next
-// block's K/V are fetched into registers while the current one is computed.
-// Gathered rows are 256-byte contiguous loads, 16 lanes per row.
+// S^T puts one query per lane: row max/sum need one cross-lane exchange and
+// the accumulator is already the P operand of the PV product.
+//
+// Pipeline: K/V blocks rotate through three LDS stages, one barrier per
+// block. While the softmax of block t runs on the VALU, the same wave issues
+// the QK MFMAs of block t+1 (independent, so the matrix core and the VALU
+// overlap); the global loads of block t+3 are in flight meanwhile. V stays
+// row-major in LDS and is read into the PV operand with the gfx950
+// transpose read (ds_read_b64_tr_b16): in each 16-lane group, output lane i,
+// element e is element i%4 of the 8-byte row addressed by lane 4e + i/4.
 #include "device.hpp"
 #include "internal.hpp"
 
 namespace mmi {
 
-constexpr int KPITCH = 136;   // bf16 per K row in LDS: 128 + 8 pad (272 B)
-constexpr int VPITCH = 68;    // bf16 per V^T row in LDS: 64 + 4 pad (136 B)
+constexpr int KPITCH = 136;   // bf16 per K row in LDS (272 B): conflict-free 16-byte operand reads
+constexpr int VPITCH = 160;   // bf16 per V row in LDS (320 B): transpose reads of 4 rows hit distinct banks
+constexpr int NSTAGE = 3;
 
-// V^T rows hold 16 groups of 4 keys; the group index is XOR-swizzled with
-// bits of the row so both the transposing writes and the operand reads
-// spread over the 64 LDS banks.
-__device__ __forceinline__ int vt_off(int d, int kgroup) { return d * VPITCH + ((kgroup ^ ((d >> 3) & 7)) << 2); }
-
-struct __align__(16) AttnSmem {
+struct __align__(16) Stage {
   uint16_t k[B * KPITCH];
-  uint16_t vt[D * VPITCH];
+  uint16_t v[B * VPITCH];
   int32_t kpos[B];
 };
 
@@ -47,75 +46,41 @@ __device__ __forceinline__ int slot_pos(const int32_t* perm, int slot, int S) {
 template <int R>
 struct Tile {
   static constexpr int NT = 128 * R;           // threads
-  static constexpr int KL = 1024 / NT;         // 16-byte K chunks loaded per thread
-  static constexpr int VG = KL >= 4 ? 4 : KL;  // keys per V unit (same 16-byte chunk of VG rows)
-  static constexpr int VU = KL / VG;           // V units per thread
+  static constexpr int L = 1024 / NT;          // 16-byte chunks of K (and of V) per thread and block
 };
 
 template <int R>
 struct BlockRegs {
-  bf16x8 k[Tile<R>::KL];
-  bf16x8 v[Tile<R>::VU * Tile<R>::VG];
+  bf16x8 k[Tile<R>::L];
+  bf16x8 v[Tile<R>::L];
 };
 
 template <int R>
 __device__ __forceinline__ void fetch_block(BlockRegs<R>& r, const AttnArgs& a, const HeadDev& hd, int jblk,
                                             int tid) {
-  using T = Tile<R>;
   const uint16_t* kb = reinterpret_cast<const uint16_t*>(a.k.p) + (int64_t)hd.kvh * a.k.sh;
   const uint16_t* vb = reinterpret_cast<const uint16_t*>(a.v.p) + (int64_t)hd.kvh * a.v.sh;
-  const int base = jblk * B;
 #pragma unroll
-  for (int it = 0; it < T::KL; ++it) {
-    const int u = tid + it * T::NT;
+  for (int it = 0; it < Tile<R>::L; ++it) {
+    const int u = tid + it * Tile<R>::NT;
     const int key = u >> 4, chunk = u & 15;
-    const int kp = slot_pos(hd.kperm, base + key, a.S);
+    const int kp = slot_pos(hd.kperm, jblk * B + key, a.S);
     r.k[it] = kp >= 0 ? load16(kb + (int64_t)kp * a.k.ss + chunk * 8) : zero8();
-  }
-#pragma unroll
-  for (int it = 0; it < T::VU; ++it) {
-    const int u = tid + it * T::NT;
-    const int kg = u >> 4, chunk = u & 15;
-#pragma unroll
-    for (int rr = 0; rr < T::VG; ++rr) {
-      const int kp = slot_pos(hd.kperm, base + kg * T::VG + rr, a.S);
-      r.v[it * T::VG + rr] = kp >= 0 ? load16(vb + (int64_t)kp * a.v.ss + chunk * 8) : zero8();
-    }
+    r.v[it] = kp >= 0 ? load16(vb + (int64_t)kp * a.v.ss + chunk * 8) : zero8();
   }
 }
 
 template <int R>
-__device__ __forceinline__ void stage_block(AttnSmem& sm, const BlockRegs<R>& r, const HeadDev& hd, int jblk,
-                                            int S, int tid) {
-  using T = Tile<R>;
+__device__ __forceinline__ void stage_block(Stage& st, const BlockRegs<R>& r, const HeadDev& hd, int jblk, int S,
+                                            int tid) {
 #pragma unroll
-  for (int it = 0; it < T::KL; ++it) {
-    const int u = tid + it * T::NT;
-    *reinterpret_cast<bf16x8*>(&sm.k[(u >> 4) * KPITCH + (u & 15) * 8]) = r.k[it];
+  for (int it = 0; it < Tile<R>::L; ++it) {
+    const int u = tid + it * Tile<R>::NT;
+    const int key = u >> 4, chunk = u & 15;
+    *reinterpret_cast<bf16x8*>(&st.k[key * KPITCH + chunk * 8]) = r.k[it];
+    *reinterpret_cast<bf16x8*>(&st.v[key * VPITCH + chunk * 8]) = r.v[it];
   }
-#pragma unroll
-  for (int it = 0; it < T::VU; ++it) {
-    const int u = tid + it * T::NT;
-    const int kg = u >> 4, chunk = u & 15;
-    const int key0 = kg * T::VG;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      uint16_t* dst = &sm.vt[vt_off(chunk * 8 + e, key0 >> 2) + (key0 & 3)];
-      if constexpr (T::VG == 4) {
-        bf16x4 t;
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) t[rr] = r.v[it * 4 + rr][e];
-        *reinterpret_cast<bf16x4*>(dst) = t;
-      } else {
-        typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
-        bf16x2 t;
-        t[0] = r.v[it * 2][e];
-        t[1] = r.v[it * 2 + 1][e];
-        *reinterpret_cast<bf16x2*>(dst) = t;
-      }
-    }
-  }
-  if (tid < B) sm.kpos[tid] = slot_pos(hd.kperm, jblk * B + tid, S);
+  if (tid < B) st.kpos[tid] = slot_pos(hd.kperm, jblk * B + tid, S);
 }
 
 // Largest key position of key block j, or INT_BIG if the block holds padding.
@@ -136,9 +101,91 @@ __device__ __forceinline__ int64_t item_of_block(int64_t b) {
   return (k / XCD_RUN) * (8 * XCD_RUN) + xcd * XCD_RUN + (k % XCD_RUN);
 }
 
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+__device__ __forceinline__ bf16x4 tr_read(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
+}
+
+// S^T tile pair (keys 0-31 and 32-63 of the block) for this wave's 32 queries.
+__device__ __forceinline__ void qk_block(const Stage& st, const bf16x8 (&qr)[8], int c, int h, f32x16 (&s)[2]) {
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int x = 0; x < 16; ++x) s[kt][x] = 0.0f;
+#pragma unroll
+  for (int st8 = 0; st8 < 8; ++st8) {
+    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&st.k[c * KPITCH + h * 64 + st8 * 8]);
+    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&st.k[(32 + c) * KPITCH + h * 64 + st8 * 8]);
+    s[0] = mfma32(k0, qr[st8], s[0]);
+    s[1] = mfma32(k1, qr[st8], s[1]);
+  }
+}
+
+__device__ __forceinline__ void mask_block(const Stage& st, int qpos, int h, f32x16 (&s)[2]) {
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int4 kp = *reinterpret_cast<const int4*>(&st.kpos[kt * 32 + 8 * i + 4 * h]);
+      if (kp.x < 0 || kp.x > qpos) s[kt][4 * i + 0] = -INFINITY;
+      if (kp.y < 0 || kp.y > qpos) s[kt][4 * i + 1] = -INFINITY;
+      if (kp.z < 0 || kp.z > qpos) s[kt][4 * i + 2] = -INFINITY;
+      if (kp.w < 0 || kp.w > qpos) s[kt][4 * i + 3] = -INFINITY;
+    }
+}
+
+// Online-softmax step: new running max, P = 2^(s*sc - m) packed to bf16
+// B operands, row sum. Returns the rescale factor (1 when the max held).
+__device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m, float& l, bf16x8 (&pb)[4],
+                                              float& alpha) {
+  float mx = NEG_BIG;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int x = 0; x < 16; ++x) mx = fmaxf(mx, s[kt][x]);
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float m_new = fmaxf(m, mx * sc);     // scale > 0: max commutes with it
+  float rs = 0.0f;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int x = 0; x < 16; ++x) {
+      const float p = fast_exp2(fmaf(s[kt][x], sc, -m_new));
+      s[kt][x] = p;
+      rs += p;
+    }
+#pragma unroll
+  for (int stp = 0; stp < 4; ++stp) {
+    const int kt = stp >> 1, half = stp & 1;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) pb[stp][x] = (__bf16)s[kt][4 * (2 * half + (x >> 2)) + (x & 3)];
+  }
+  rs += __shfl_xor(rs, 32);
+  alpha = fast_exp2(m - m_new);
+  l = l * alpha + rs;
+  m = m_new;
+}
+
+// O^T += V^T P^T; the V^T operand comes from row-major V by transpose reads.
+__device__ __forceinline__ void pv_block(const Stage& st, const bf16x8 (&pb)[4], int vlane, f32x16 (&o)[4]) {
+#pragma unroll
+  for (int stp = 0; stp < 4; ++stp) {
+    const int kt = stp >> 1, half = stp & 1;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const uint16_t* p0 = &st.v[vlane + (32 * kt + 16 * half) * VPITCH + 32 * dt];
+      const bf16x4 lo = tr_read(p0);
+      const bf16x4 hi = tr_read(p0 + 8 * VPITCH);
+      const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      o[dt] = mfma32(va, pb[stp], o[dt]);
+    }
+  }
+}
+
 template <int R>
-__global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(2))) void k_attention(AttnArgs a) {
-  __shared__ AttnSmem sm;
+__global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 ? 2 : 1))) void k_attention(AttnArgs a) {
+  __shared__ Stage stg[NSTAGE];
   const int64_t it = item_of_block(blockIdx.x);
   if (it >= a.nitems) return;
   const WorkItem w = a.items[it];
@@ -158,6 +205,9 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
     for (int s = 0; s < 8; ++s) qr[s] = qpos >= 0 ? load16(row + 8 * s) : zero8();
   }
+  // transpose-read source row/column of this lane inside a V stage
+  const int grp = lane >> 4, li = lane & 15;
+  const int vlane = (4 * (grp >> 1) + (li >> 2)) * VPITCH + 16 * (grp & 1) + 4 * (li & 3);
 
   f32x16 o[4];
 #pragma unroll
@@ -167,86 +217,66 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(2))) vo
   float m = NEG_BIG, l = 0.0f;
   const float sc = 0.08838834764831845f * LOG2E;   // sqrt(1/128) * log2(e)
 
+  const int n = w.e1 - w.e0;
+  const int32_t* ent = hd.gcol + w.e0;
   BlockRegs<R> regs;
-  fetch_block<R>(regs, a, hd, hd.gcol[w.e0] & 0xffff, tid);
-  for (int e = w.e0; e < w.e1; ++e) {
-    const int ent = hd.gcol[e];
-    const int jcur = ent & 0xffff;
-    stage_block<R>(sm, regs, hd, jcur, a.S, tid);
-    __syncthreads();
-    if (e + 1 < w.e1) fetch_block<R>(regs, a, hd, hd.gcol[e + 1] & 0xffff, tid);
-    if ((ent >> (16 + rb)) & 1) {          // this wave's query block selected key block jcur
-      const bool need_mask = block_kmax(hd, jcur, a.S) > qmin;   // wave-uniform
-      f32x16 s[2];
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int x = 0; x < 16; ++x) s[kt][x] = 0.0f;
-#pragma unroll
-      for (int st = 0; st < 8; ++st) {
-        const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&sm.k[c * KPITCH + h * 64 + st * 8]);
-        const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&sm.k[(32 + c) * KPITCH + h * 64 + st * 8]);
-        s[0] = mfma32(k0, qr[st], s[0]);
-        s[1] = mfma32(k1, qr[st], s[1]);
-      }
-      if (need_mask) {
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int4 kp = *reinterpret_cast<const int4*>(&sm.kpos[kt * 32 + 8 * i + 4 * h]);
-            if (kp.x < 0 || kp.x > qpos) s[kt][4 * i + 0] = -INFINITY;
-            if (kp.y < 0 || kp.y > qpos) s[kt][4 * i + 1] = -INFINITY;
-            if (kp.z < 0 || kp.z > qpos) s[kt][4 * i + 2] = -INFINITY;
-            if (kp.w < 0 || kp.w > qpos) s[kt][4 * i + 3] = -INFINITY;
-          }
-      }
-      float mx = NEG_BIG;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int x = 0; x < 16; ++x) mx = fmaxf(mx, s[kt][x]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m, mx * sc);     // scale > 0: max commutes with it
-      float rs = 0.0f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int x = 0; x < 16; ++x) {
-          const float p = fast_exp2(fmaf(s[kt][x], sc, -m_new));
-          s[kt][x] = p;
-          rs += p;
-        }
-      rs += __shfl_xor(rs, 32);
-      if (__any(m_new != m)) {   // rescale only when some row's running max moved
-        const float alpha = fast_exp2(m - m_new);
-        l *= alpha;
+  int e_cur = ent[0];
+  fetch_block<R>(regs, a, hd, e_cur & 0xffff, tid);
+  stage_block<R>(stg[0], regs, hd, e_cur & 0xffff, a.S, tid);
+  int e_nxt = n > 1 ? ent[1] : 0;
+  if (n > 1) {
+    fetch_block<R>(regs, a, hd, e_nxt & 0xffff, tid);
+    stage_block<R>(stg[1], regs, hd, e_nxt & 0xffff, a.S, tid);
+  }
+  int e_far = n > 2 ? ent[2] : 0;
+  if (n > 2) fetch_block<R>(regs, a, hd, e_far & 0xffff, tid);
+  __syncthreads();
+
+  f32x16 s_cur[2], s_nxt[2];
+  bool act_cur = (e_cur >> (16 + rb)) & 1;
+  if (act_cur) qk_block(stg[0], qr, c, h, s_cur);
+  int cs = 0;                                   // stage of block t
+  for (int t = 0; t < n; ++t) {
+    const int ns = cs == NSTAGE - 1 ? 0 : cs + 1;
+    const bool act_nxt = t + 1 < n && ((e_nxt >> (16 + rb)) & 1);
+    if (act_cur && block_kmax(hd, e_cur & 0xffff, a.S) > qmin) mask_block(stg[cs], qpos, h, s_cur);
+    bf16x8 pb[4];
+    float alpha = 1.0f;
+    if (act_cur && act_nxt) {
+      // QK MFMAs of block t+1 are independent of the softmax of block t
+      qk_block(stg[ns], qr, c, h, s_nxt);
+      softmax_block(s_cur, sc, m, l, pb, alpha);
+    } else {
+      if (act_nxt) qk_block(stg[ns], qr, c, h, s_nxt);
+      if (act_cur) softmax_block(s_cur, sc, m, l, pb, alpha);
+    }
+    if (act_cur) {
+      if (__any(alpha != 1.0f)) {
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
           for (int x = 0; x < 16; ++x) o[dt][x] *= alpha;
       }
-      l += rs;
-      m = m_new;
-#pragma unroll
-      for (int st = 0; st < 4; ++st) {
-        const int kt = st >> 1, half = st & 1;
-        bf16x8 pb;
-#pragma unroll
-        for (int x = 0; x < 8; ++x) pb[x] = (__bf16)s[kt][4 * (2 * half + (x >> 2)) + (x & 3)];
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) {
-          const int d = 32 * dt + c, g = 8 * kt + 4 * half + h;
-          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&sm.vt[vt_off(d, g)]);
-          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&sm.vt[vt_off(d, g + 2)]);
-          bf16x8 va;
-#pragma unroll
-          for (int x = 0; x < 4; ++x) { va[x] = lo[x]; va[4 + x] = hi[x]; }
-          o[dt] = mfma32(va, pb, o[dt]);
-        }
+      pv_block(stg[cs], pb, vlane, o);
+    }
+    if (t + 2 < n) {
+      const int fs = ns == NSTAGE - 1 ? 0 : ns + 1;
+      stage_block<R>(stg[fs], regs, hd, e_far & 0xffff, a.S, tid);
+      if (t + 3 < n) {
+        const int e3 = ent[t + 3];
+        fetch_block<R>(regs, a, hd, e3 & 0xffff, tid);
+        e_cur = e_nxt; e_nxt = e_far; e_far = e3;
+      } else {
+        e_cur = e_nxt; e_nxt = e_far; e_far = 0;
       }
+    } else {
+      e_cur = e_nxt; e_nxt = e_far; e_far = 0;
     }
     __syncthreads();
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) s_cur[kt] = s_nxt[kt];
+    act_cur = act_nxt;
+    cs = ns;
   }
 
   if (w.part < 0) {
