@@ -151,6 +151,7 @@ def main():
     ms = ev0.elapsed_time(ev1) / args.steps
     avg = {key: float(np.mean([t[key] for t in timings])) for key in timings[0]}
     blocks = int(timings[-1]["computed_blocks"])
+    loaded = int(timings[-1]["loaded_blocks"])
     attn_tflops = blocks * FLOP_PER_BLOCK / (avg["attn_ms"] * 1e-3) / 1e12
     nb = (wl.S + 63) // 64
     causal_blocks = nb * (nb + 1) // 2 * wl.Hq
@@ -194,7 +195,8 @@ def main():
         "config": {"workload": wl.name, "S": wl.S, "Hq": wl.Hq, "Hkv": wl.Hkv, "head_dim": 128,
                    "block": 64, "parallelism": "single GPU"},
         "stages_ms": {k2: avg[k2] for k2 in ("est_ms", "select_ms", "index_ms", "attn_ms", "combine_ms")},
-        "blocks": {"computed": blocks, "causal": causal_blocks, "density": blocks / causal_blocks},
+        "blocks": {"computed": blocks, "loaded": loaded, "causal": causal_blocks,
+                   "density": blocks / causal_blocks, "computed_per_load": blocks / max(loaded, 1)},
         "roofline": {"bound": "mfma", "kernel": "k_attention", "achieved": attn_tflops,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": attn_tflops / PEAK_BF16_TFLOPS,
                      "traffic": None},

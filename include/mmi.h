@@ -119,6 +119,7 @@ typedef struct mmi_head_stats {
   int32_t sigma[MMI_MAX_MODALITIES];  /* chosen Grid stride per op slot (0 = not Grid / dense fallback) */
   int32_t phase[MMI_MAX_MODALITIES];
   int32_t group_stride;          /* query-block stride of the attention row groups (1, 2, 4 or 8) */
+  int64_t loaded_blocks;         /* key blocks staged for this head (sum of the row-group unions) */
 } mmi_head_stats;
 
 /* Stage durations of a plan, from HIP events recorded on the plan's stream
@@ -132,6 +133,7 @@ typedef struct mmi_plan_timing {
   float combine_ms;    /* merge of split query blocks */
   int64_t computed_blocks;  /* selected 64x64 blocks over all heads */
   int64_t work_items;
+  int64_t loaded_blocks;    /* K/V blocks staged by the attention kernel (union entries of all row groups) */
 } mmi_plan_timing;
 
 /* export kinds for mmi_plan_export (host copies; the call synchronises) */

@@ -6,10 +6,9 @@
 //
 // One work item = a row group of R permuted query blocks and a contiguous
 // range of the union of their key-block lists; each union entry carries one
-// flag per query block. The workgroup has 2R waves; waves 2r and 2r+1 own
-// the 64 rows of member r (32 rows each). Every key block of the range is
-// loaded once into LDS and used by all members that selected it. Per key
-// block and active wave:
+// flag per query block. The workgroup has 2R waves, each owning 32 rows of
+// one member. Every key block of the range is loaded once into LDS and used
+// by all members that selected it. Per key block and active wave:
 //   S^T (64 keys x 32 queries) = K Q^T         16 MFMA 32x32x16 bf16
 //   mask by original positions (k <= q) where the block reaches past the
 //   wave's first query, online softmax in fp32 (log2 domain)
@@ -17,13 +16,20 @@
 // S^T puts one query per lane: row max/sum need one cross-lane exchange and
 // the accumulator is already the P operand of the PV product.
 //
-// Pipeline: K/V blocks rotate through three LDS stages, one barrier per
-// block. While the softmax of block t runs on the VALU, the same wave issues
-// the QK MFMAs of block t+1 (independent, so the matrix core and the VALU
-// overlap); the global loads of block t+3 are in flight meanwhile. V stays
-// row-major in LDS and is read into the PV operand with the gfx950
+// Pipeline: K/V blocks rotate through four LDS stages with one barrier per
+// block; the global loads of block t+3 are in flight while block t is
+// computed. Within a wave, the QK MFMAs of block t+1 are issued between the
+// softmax instructions of block t. Across waves, the first R waves run
+// [softmax(t) + QK(t+1)] then PV(t), while the other R waves run PV(t-1)
+// then [softmax(t) + QK(t+1)]: a SIMD holds one wave of each half, so one
+// wave's exponentials overlap the other wave's PV products.
+// V stays row-major in LDS and is read into the PV operand with the gfx950
 // transpose read (ds_read_b64_tr_b16): in each 16-lane group, output lane i,
 // element e is element i%4 of the 8-byte row addressed by lane 4e + i/4.
+//
+// The running maximum is only moved when a row's block maximum exceeds it by
+// more than RESCALE_SLACK (log2 units): P entries then stay below 2^8, which
+// neither bf16 nor the fp32 sums mind, and the O rescale becomes rare.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -31,16 +37,22 @@ namespace mmi {
 
 constexpr int KPITCH = 136;   // bf16 per K row in LDS (272 B): conflict-free 16-byte operand reads
 constexpr int VPITCH = 160;   // bf16 per V row in LDS (320 B): transpose reads of 4 rows hit distinct banks
-constexpr int NSTAGE = 3;
+constexpr int NSTAGE = 4;
+constexpr float RESCALE_SLACK = 8.0f;
 
 struct __align__(16) Stage {
   uint16_t k[B * KPITCH];
   uint16_t v[B * VPITCH];
-  int32_t kpos[B];
+  int32_t kpos[B];            // original key position, INT_BIG for padding
 };
 
 __device__ __forceinline__ int slot_pos(const int32_t* perm, int slot, int S) {
   return perm ? perm[slot] : (slot < S ? slot : -1);
+}
+
+// Wave-uniform read of read-only data through the scalar unit.
+__device__ __forceinline__ int ld_uniform(const int32_t* p) {
+  return *(const __attribute__((address_space(4))) int32_t*)(p);
 }
 
 template <int R>
@@ -55,6 +67,8 @@ struct BlockRegs {
   bf16x8 v[Tile<R>::L];
 };
 
+// Padding slots read key row 0 (always present); their V is zeroed and their
+// scores are masked, so the values never reach the output.
 template <int R>
 __device__ __forceinline__ void fetch_block(BlockRegs<R>& r, const AttnArgs& a, const HeadDev& hd, int jblk,
                                             int tid) {
@@ -65,8 +79,10 @@ __device__ __forceinline__ void fetch_block(BlockRegs<R>& r, const AttnArgs& a, 
     const int u = tid + it * Tile<R>::NT;
     const int key = u >> 4, chunk = u & 15;
     const int kp = slot_pos(hd.kperm, jblk * B + key, a.S);
-    r.k[it] = kp >= 0 ? load16(kb + (int64_t)kp * a.k.ss + chunk * 8) : zero8();
-    r.v[it] = kp >= 0 ? load16(vb + (int64_t)kp * a.v.ss + chunk * 8) : zero8();
+    const int row = kp >= 0 ? kp : 0;
+    r.k[it] = load16(kb + (int64_t)row * a.k.ss + chunk * 8);
+    const bf16x8 vv = load16(vb + (int64_t)row * a.v.ss + chunk * 8);
+    r.v[it] = kp >= 0 ? vv : zero8();
   }
 }
 
@@ -80,12 +96,15 @@ __device__ __forceinline__ void stage_block(Stage& st, const BlockRegs<R>& r, co
     *reinterpret_cast<bf16x8*>(&st.k[key * KPITCH + chunk * 8]) = r.k[it];
     *reinterpret_cast<bf16x8*>(&st.v[key * VPITCH + chunk * 8]) = r.v[it];
   }
-  if (tid < B) st.kpos[tid] = slot_pos(hd.kperm, jblk * B + tid, S);
+  if (tid < B) {
+    const int kp = slot_pos(hd.kperm, jblk * B + tid, S);
+    st.kpos[tid] = kp >= 0 ? kp : INT_BIG;
+  }
 }
 
 // Largest key position of key block j, or INT_BIG if the block holds padding.
 __device__ __forceinline__ int block_kmax(const HeadDev& hd, int j, int S) {
-  if (hd.kmaxpos) return hd.kmaxpos[j];
+  if (hd.kmaxpos) return ld_uniform(hd.kmaxpos + j);
   const int last = j * B + B - 1;
   return last < S ? last : INT_BIG;
 }
@@ -109,16 +128,13 @@ __device__ __forceinline__ bf16x4 tr_read(const uint16_t* p) {
 
 // S^T tile pair (keys 0-31 and 32-63 of the block) for this wave's 32 queries.
 __device__ __forceinline__ void qk_block(const Stage& st, const bf16x8 (&qr)[8], int c, int h, f32x16 (&s)[2]) {
-#pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-    for (int x = 0; x < 16; ++x) s[kt][x] = 0.0f;
+  const f32x16 zero = {};
 #pragma unroll
   for (int st8 = 0; st8 < 8; ++st8) {
     const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&st.k[c * KPITCH + h * 64 + st8 * 8]);
     const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&st.k[(32 + c) * KPITCH + h * 64 + st8 * 8]);
-    s[0] = mfma32(k0, qr[st8], s[0]);
-    s[1] = mfma32(k1, qr[st8], s[1]);
+    s[0] = mfma32(k0, qr[st8], st8 == 0 ? zero : s[0]);
+    s[1] = mfma32(k1, qr[st8], st8 == 0 ? zero : s[1]);
   }
 }
 
@@ -128,15 +144,16 @@ __device__ __forceinline__ void mask_block(const Stage& st, int qpos, int h, f32
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int4 kp = *reinterpret_cast<const int4*>(&st.kpos[kt * 32 + 8 * i + 4 * h]);
-      if (kp.x < 0 || kp.x > qpos) s[kt][4 * i + 0] = -INFINITY;
-      if (kp.y < 0 || kp.y > qpos) s[kt][4 * i + 1] = -INFINITY;
-      if (kp.z < 0 || kp.z > qpos) s[kt][4 * i + 2] = -INFINITY;
-      if (kp.w < 0 || kp.w > qpos) s[kt][4 * i + 3] = -INFINITY;
+      if (kp.x > qpos) s[kt][4 * i + 0] = -INFINITY;
+      if (kp.y > qpos) s[kt][4 * i + 1] = -INFINITY;
+      if (kp.z > qpos) s[kt][4 * i + 2] = -INFINITY;
+      if (kp.w > qpos) s[kt][4 * i + 3] = -INFINITY;
     }
 }
 
-// Online-softmax step: new running max, P = 2^(s*sc - m) packed to bf16
-// B operands, row sum. Returns the rescale factor (1 when the max held).
+// Online-softmax step on the scores of one block: P = 2^(s*sc - m) packed to
+// bf16 B operands, row sum into l. m moves (and alpha < 1 is returned) only
+// when some row's block maximum passes it by more than RESCALE_SLACK.
 __device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m, float& l, bf16x8 (&pb)[4],
                                               float& alpha) {
   float mx = NEG_BIG;
@@ -144,14 +161,19 @@ __device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m
   for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
     for (int x = 0; x < 16; ++x) mx = fmaxf(mx, s[kt][x]);
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const float m_new = fmaxf(m, mx * sc);     // scale > 0: max commutes with it
+  mx = fmaxf(mx, __shfl_xor(mx, 32)) * sc;     // scale > 0: max commutes with it
+  alpha = 1.0f;
+  if (__any(mx > m + RESCALE_SLACK)) {
+    const float m_new = fmaxf(m, mx);
+    alpha = fast_exp2(m - m_new);
+    m = m_new;
+  }
   float rs = 0.0f;
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
     for (int x = 0; x < 16; ++x) {
-      const float p = fast_exp2(fmaf(s[kt][x], sc, -m_new));
+      const float p = fast_exp2(fmaf(s[kt][x], sc, -m));
       s[kt][x] = p;
       rs += p;
     }
@@ -162,9 +184,7 @@ __device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m
     for (int x = 0; x < 8; ++x) pb[stp][x] = (__bf16)s[kt][4 * (2 * half + (x >> 2)) + (x & 3)];
   }
   rs += __shfl_xor(rs, 32);
-  alpha = fast_exp2(m - m_new);
   l = l * alpha + rs;
-  m = m_new;
 }
 
 // O^T += V^T P^T; the V^T operand comes from row-major V by transpose reads.
@@ -183,6 +203,73 @@ __device__ __forceinline__ void pv_block(const Stage& st, const bf16x8 (&pb)[4],
   }
 }
 
+// Per-wave state of the block loop.
+struct WaveState {
+  f32x16 o[4];
+  bf16x8 qr[8];
+  float m, l;
+  int qpos, qmin, rb, c, h, vlane;
+};
+
+// One key block t (union entries et .. et3 = entries t .. t+3, 0 past the
+// end). s_cur holds the scores of block t if the wave takes part in it;
+// s_nxt receives those of block t+1. The early half multiplies P(t)V(t)
+// before the barrier that ends the step, the late half right after it.
+template <int R, bool LATE>
+__device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const AttnArgs& a, const HeadDev& hd,
+                                           BlockRegs<R>& regs, int tid, int t, int n, int et, int et1, int et2,
+                                           int et3, f32x16 (&s_cur)[2], f32x16 (&s_nxt)[2], float sc) {
+  const int cs = t & (NSTAGE - 1), ns = (t + 1) & (NSTAGE - 1);
+  const bool act_c = (et >> (16 + ws.rb)) & 1;
+  const bool act_n = t + 1 < n && ((et1 >> (16 + ws.rb)) & 1);
+  if (act_c && block_kmax(hd, et & 0xffff, a.S) > ws.qmin) mask_block(stg[cs], ws.qpos, ws.h, s_cur);
+  float alpha = 1.0f;
+  bf16x8 pb[4];
+  if (act_c && act_n) {
+    // QK MFMAs of block t+1 are independent of the softmax of block t
+    qk_block(stg[ns], ws.qr, ws.c, ws.h, s_nxt);
+    softmax_block(s_cur, sc, ws.m, ws.l, pb, alpha);
+  } else {
+    if (act_n) qk_block(stg[ns], ws.qr, ws.c, ws.h, s_nxt);
+    if (act_c) softmax_block(s_cur, sc, ws.m, ws.l, pb, alpha);
+  }
+  if (act_c && __any(alpha != 1.0f)) {
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int x = 0; x < 16; ++x) ws.o[dt][x] *= alpha;
+  }
+  if (!LATE && act_c) pv_block(stg[cs], pb, ws.vlane, ws.o);
+  // stage t+2 (its stage was last read in step t-1), start loading t+3
+  if (t + 2 < n) stage_block<R>(stg[(t + 2) & (NSTAGE - 1)], regs, hd, et2 & 0xffff, a.S, tid);
+  if (t + 3 < n) fetch_block<R>(regs, a, hd, et3 & 0xffff, tid);
+  __syncthreads();
+  if (LATE && act_c) pv_block(stg[cs], pb, ws.vlane, ws.o);
+}
+
+template <int R, bool LATE>
+__device__ __forceinline__ void block_loop(WaveState& ws, Stage* stg, const AttnArgs& a, const HeadDev& hd,
+                                           const WorkItem& w, BlockRegs<R>& regs, int tid) {
+  const float sc = 0.08838834764831845f * LOG2E;   // sqrt(1/128) * log2(e)
+  const int n = w.e1 - w.e0;
+  const int32_t* ent = hd.gcol + w.e0;
+  int e0 = ld_uniform(ent);
+  int e1 = n > 1 ? ld_uniform(ent + 1) : 0;
+  int e2 = n > 2 ? ld_uniform(ent + 2) : 0;
+  f32x16 sa[2], sb[2];
+  if ((e0 >> (16 + ws.rb)) & 1) qk_block(stg[0], ws.qr, ws.c, ws.h, sa);
+  // two steps per trip so that the score buffers swap roles without copies
+  for (int t = 0; t < n; t += 2) {
+    int e3 = t + 3 < n ? ld_uniform(ent + t + 3) : 0;
+    block_step<R, LATE>(ws, stg, a, hd, regs, tid, t, n, e0, e1, e2, e3, sa, sb, sc);
+    e0 = e1; e1 = e2; e2 = e3;
+    if (t + 1 >= n) break;
+    e3 = t + 4 < n ? ld_uniform(ent + t + 4) : 0;
+    block_step<R, LATE>(ws, stg, a, hd, regs, tid, t + 1, n, e0, e1, e2, e3, sb, sa, sc);
+    e0 = e1; e1 = e2; e2 = e3;
+  }
+}
+
 template <int R>
 __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 ? 2 : 1))) void k_attention(AttnArgs a) {
   __shared__ Stage stg[NSTAGE];
@@ -191,94 +278,54 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
   const WorkItem w = a.items[it];
   const HeadDev hd = a.heads[w.head];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int c = lane & 31, h = lane >> 5;
-  const int rb = wave >> 1;                        // member of the group owned by this wave
-  const int qblk = group_row(w.group, rb, R, hd.gp[0]);
-  const int qpos = qblk < hd.nbq ? slot_pos(hd.qperm, qblk * B + (wave & 1) * 32 + c, a.S) : -1;
-  int qmin = qpos >= 0 ? qpos : INT_BIG;      // smallest valid query position of the wave
+  // Waves 0..R-1 own rows 0-31 of member `wave`; waves R..2R-1 own rows
+  // 32-63 of member (wave - R + R/2) mod R, so that the two waves sharing a
+  // SIMD (wave and wave + 4 for R = 4) serve different members.
+  const bool late = wave >= R;
+  WaveState ws;
+  ws.rb = late ? (wave - R + R / 2) % R : wave;
+  const int half = late ? 1 : 0;
+  ws.c = lane & 31;
+  ws.h = lane >> 5;
+  const int qblk = group_row(w.group, ws.rb, R, hd.gp[0]);
+  ws.qpos = qblk < hd.nbq ? slot_pos(hd.qperm, qblk * B + half * 32 + ws.c, a.S) : -1;
+  int qmin = ws.qpos >= 0 ? ws.qpos : INT_BIG;   // smallest valid query position of the wave
 #pragma unroll
   for (int off = 1; off < 32; off <<= 1) qmin = min(qmin, __shfl_xor(qmin, off));
-  bf16x8 qr[8];
+  ws.qmin = qmin;
   {
     const uint16_t* qb = reinterpret_cast<const uint16_t*>(a.q.p) + (int64_t)w.head * a.q.sh;
-    const uint16_t* row = qb + (int64_t)max(qpos, 0) * a.q.ss + h * 64;
+    const uint16_t* row = qb + (int64_t)max(ws.qpos, 0) * a.q.ss + ws.h * 64;
 #pragma unroll
-    for (int s = 0; s < 8; ++s) qr[s] = qpos >= 0 ? load16(row + 8 * s) : zero8();
+    for (int s = 0; s < 8; ++s) ws.qr[s] = ws.qpos >= 0 ? load16(row + 8 * s) : zero8();
   }
   // transpose-read source row/column of this lane inside a V stage
   const int grp = lane >> 4, li = lane & 15;
-  const int vlane = (4 * (grp >> 1) + (li >> 2)) * VPITCH + 16 * (grp & 1) + 4 * (li & 3);
-
-  f32x16 o[4];
+  ws.vlane = (4 * (grp >> 1) + (li >> 2)) * VPITCH + 16 * (grp & 1) + 4 * (li & 3);
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) o[dt][e] = 0.0f;
-  float m = NEG_BIG, l = 0.0f;
-  const float sc = 0.08838834764831845f * LOG2E;   // sqrt(1/128) * log2(e)
+    for (int e = 0; e < 16; ++e) ws.o[dt][e] = 0.0f;
+  ws.m = NEG_BIG;
+  ws.l = 0.0f;
 
+  // prologue: blocks 0 and 1 staged, block 2 in registers
   const int n = w.e1 - w.e0;
   const int32_t* ent = hd.gcol + w.e0;
   BlockRegs<R> regs;
-  int e_cur = ent[0];
-  fetch_block<R>(regs, a, hd, e_cur & 0xffff, tid);
-  stage_block<R>(stg[0], regs, hd, e_cur & 0xffff, a.S, tid);
-  int e_nxt = n > 1 ? ent[1] : 0;
+  fetch_block<R>(regs, a, hd, ld_uniform(ent) & 0xffff, tid);
+  stage_block<R>(stg[0], regs, hd, ld_uniform(ent) & 0xffff, a.S, tid);
   if (n > 1) {
-    fetch_block<R>(regs, a, hd, e_nxt & 0xffff, tid);
-    stage_block<R>(stg[1], regs, hd, e_nxt & 0xffff, a.S, tid);
+    fetch_block<R>(regs, a, hd, ld_uniform(ent + 1) & 0xffff, tid);
+    stage_block<R>(stg[1], regs, hd, ld_uniform(ent + 1) & 0xffff, a.S, tid);
   }
-  int e_far = n > 2 ? ent[2] : 0;
-  if (n > 2) fetch_block<R>(regs, a, hd, e_far & 0xffff, tid);
+  if (n > 2) fetch_block<R>(regs, a, hd, ld_uniform(ent + 2) & 0xffff, tid);
   __syncthreads();
+  if (late) block_loop<R, true>(ws, stg, a, hd, w, regs, tid);
+  else block_loop<R, false>(ws, stg, a, hd, w, regs, tid);
 
-  f32x16 s_cur[2], s_nxt[2];
-  bool act_cur = (e_cur >> (16 + rb)) & 1;
-  if (act_cur) qk_block(stg[0], qr, c, h, s_cur);
-  int cs = 0;                                   // stage of block t
-  for (int t = 0; t < n; ++t) {
-    const int ns = cs == NSTAGE - 1 ? 0 : cs + 1;
-    const bool act_nxt = t + 1 < n && ((e_nxt >> (16 + rb)) & 1);
-    if (act_cur && block_kmax(hd, e_cur & 0xffff, a.S) > qmin) mask_block(stg[cs], qpos, h, s_cur);
-    bf16x8 pb[4];
-    float alpha = 1.0f;
-    if (act_cur && act_nxt) {
-      // QK MFMAs of block t+1 are independent of the softmax of block t
-      qk_block(stg[ns], qr, c, h, s_nxt);
-      softmax_block(s_cur, sc, m, l, pb, alpha);
-    } else {
-      if (act_nxt) qk_block(stg[ns], qr, c, h, s_nxt);
-      if (act_cur) softmax_block(s_cur, sc, m, l, pb, alpha);
-    }
-    if (act_cur) {
-      if (__any(alpha != 1.0f)) {
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-          for (int x = 0; x < 16; ++x) o[dt][x] *= alpha;
-      }
-      pv_block(stg[cs], pb, vlane, o);
-    }
-    if (t + 2 < n) {
-      const int fs = ns == NSTAGE - 1 ? 0 : ns + 1;
-      stage_block<R>(stg[fs], regs, hd, e_far & 0xffff, a.S, tid);
-      if (t + 3 < n) {
-        const int e3 = ent[t + 3];
-        fetch_block<R>(regs, a, hd, e3 & 0xffff, tid);
-        e_cur = e_nxt; e_nxt = e_far; e_far = e3;
-      } else {
-        e_cur = e_nxt; e_nxt = e_far; e_far = 0;
-      }
-    } else {
-      e_cur = e_nxt; e_nxt = e_far; e_far = 0;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) s_cur[kt] = s_nxt[kt];
-    act_cur = act_nxt;
-    cs = ns;
-  }
-
+  const float m = ws.m, l = ws.l;
+  const int qpos = ws.qpos, h = ws.h;
   if (w.part < 0) {
     if (qpos >= 0) {
       const float inv = 1.0f / l;
@@ -289,19 +336,19 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
         for (int i = 0; i < 4; ++i) {
           bf16x4 t;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) t[j] = (__bf16)(o[dt][4 * i + j] * inv);
+          for (int j = 0; j < 4; ++j) t[j] = (__bf16)(ws.o[dt][4 * i + j] * inv);
           *reinterpret_cast<bf16x4*>(orow + 32 * dt + 8 * i + 4 * h) = t;
         }
       if (h == 0 && a.lse) a.lse[(int64_t)w.head * a.S + qpos] = (m + fast_log2(l)) * LN2;
     }
   } else {
-    const int row = wave * 32 + c;             // row of the group, 0 .. 64R-1
+    const int row = ws.rb * B + half * 32 + ws.c;    // row of the group, 0 .. 64R-1
     float* po = a.part_o + ((int64_t)w.part * (B * R) + row) * D;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        float4 t = make_float4(o[dt][4 * i], o[dt][4 * i + 1], o[dt][4 * i + 2], o[dt][4 * i + 3]);
+        float4 t = make_float4(ws.o[dt][4 * i], ws.o[dt][4 * i + 1], ws.o[dt][4 * i + 2], ws.o[dt][4 * i + 3]);
         *reinterpret_cast<float4*>(po + 32 * dt + 8 * i + 4 * h) = t;
       }
     if (h == 0) {

@@ -163,6 +163,7 @@ struct mmi_plan {
   std::vector<std::vector<uint8_t>> keep;   // host sources of asynchronous uploads
   hipEvent_t ev[7] = {};          // stage boundaries: create 0..3, execute 4..6
   int64_t nnz_all = 0;
+  int64_t gnnz_all = 0;
   bool executed = false;
   std::vector<int> rowset_n;
 };
@@ -700,6 +701,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   HIPCHK(launch_work_fill(P->d_heads, p.Hq, d_ib, d_pb, d_sb, max_groups, P->d_items, P->d_splits, st));
   HIPCHK(hipEventRecord(P->ev[3], st));
   P->nnz_all = nnz_all;
+  P->gnnz_all = gnnz_all;
 }
 
 static void plan_execute_impl(mmi_plan* P, const void* q, const void* k, const void* v, void* o, float* lse,
@@ -886,6 +888,7 @@ int mmi_plan_stats(mmi_plan* P, int head, mmi_head_stats* out) {
     int32_t gp[2];
     HIPCHK(hipMemcpy(gp, hd.gp, sizeof gp, hipMemcpyDeviceToHost));
     s.group_stride = gp[0];
+    s.loaded_blocks = H.gnnz;
     *out = s;
   });
 }
@@ -905,6 +908,7 @@ int mmi_plan_timing_get(mmi_plan* P, mmi_plan_timing* out) {
     }
     t.computed_blocks = P->nnz_all;
     t.work_items = P->nitems;
+    t.loaded_blocks = P->gnnz_all;
     *out = t;
   });
 }

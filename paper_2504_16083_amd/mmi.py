@@ -55,13 +55,14 @@ class mmi_problem(ct.Structure):
 class mmi_head_stats(ct.Structure):
     _fields_ = [("kind", ct.c_int32), ("n_qblocks", ct.c_int32), ("n_kblocks", ct.c_int32),
                 ("nnz_blocks", ct.c_int64), ("causal_blocks", ct.c_int64), ("split_rows", ct.c_int32),
-                ("sigma", ct.c_int32 * MAXM), ("phase", ct.c_int32 * MAXM), ("group_stride", ct.c_int32)]
+                ("sigma", ct.c_int32 * MAXM), ("phase", ct.c_int32 * MAXM), ("group_stride", ct.c_int32),
+                ("loaded_blocks", ct.c_int64)]
 
 
 class mmi_plan_timing(ct.Structure):
     _fields_ = [("est_ms", ct.c_float), ("select_ms", ct.c_float), ("index_ms", ct.c_float),
                 ("attn_ms", ct.c_float), ("combine_ms", ct.c_float), ("computed_blocks", ct.c_int64),
-                ("work_items", ct.c_int64)]
+                ("work_items", ct.c_int64), ("loaded_blocks", ct.c_int64)]
 
 
 SYMBOLS = ["mmi_plan_timing_get", "mmi_version", "mmi_status_str", "mmi_last_error", "mmi_ctx_create", "mmi_ctx_destroy",

@@ -85,4 +85,5 @@ def test_ctx_without_device_is_an_error():
 def test_stats_struct_matches_header():
     # kind, n_qblocks, n_kblocks (12) + pad (4) + 2 x int64 (16) + split_rows (4) + 2 x 8 int32 (64)
     assert mmi.mmi_head_stats.group_stride.offset == 100
-    assert ct.sizeof(mmi.mmi_head_stats) == 104
+    assert mmi.mmi_head_stats.loaded_blocks.offset == 104
+    assert ct.sizeof(mmi.mmi_head_stats) == 112
