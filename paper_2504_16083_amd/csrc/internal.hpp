@@ -103,7 +103,7 @@ struct HeadDev {
   int32_t* gp;                // [2] chosen row stride rho of the groups, number of groups
   int32_t* gcount;            // [groups] union sizes
   int32_t* growptr;           // [ngroups+1]
-  int32_t* gcol;              // [gnnz]
+  int32_t* gcol;              // [gnnz] union entries: key block, select flags << 16, mask flags << 24
   int32_t* chunklen;          // [1] union entries per work item for this head (set by the scan)
   int32_t* chunks;            // [ngroups] work items per group
   int32_t* itembase;          // [ngroups] exclusive prefix of chunks

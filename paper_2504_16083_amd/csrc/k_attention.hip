@@ -46,13 +46,14 @@ struct __align__(16) Stage {
   int32_t kpos[B];            // original key position, INT_BIG for padding
 };
 
-__device__ __forceinline__ int slot_pos(const int32_t* perm, int slot, int S) {
-  return perm ? perm[slot] : (slot < S ? slot : -1);
+// Load of plan data through a global-address-space pointer (a generic one
+// would become a flat load, which also counts against the LDS wait counter).
+__device__ __forceinline__ int ld_global(const int32_t* p) {
+  return *(const __attribute__((address_space(1))) int32_t*)(p);
 }
 
-// Wave-uniform read of read-only data through the scalar unit.
-__device__ __forceinline__ int ld_uniform(const int32_t* p) {
-  return *(const __attribute__((address_space(4))) int32_t*)(p);
+__device__ __forceinline__ int slot_pos(const int32_t* perm, int slot, int S) {
+  return perm ? ld_global(perm + slot) : (slot < S ? slot : -1);
 }
 
 template <int R>
@@ -65,49 +66,69 @@ template <int R>
 struct BlockRegs {
   bf16x8 k[Tile<R>::L];
   bf16x8 v[Tile<R>::L];
+  int kp[Tile<R>::L];          // original positions of the thread's keys (-1 = padding)
 };
 
-// Padding slots read key row 0 (always present); their V is zeroed and their
-// scores are masked, so the values never reach the output.
+// Original positions of the keys this thread loads from key block jblk.
 template <int R>
-__device__ __forceinline__ void fetch_block(BlockRegs<R>& r, const AttnArgs& a, const HeadDev& hd, int jblk,
-                                            int tid) {
+__device__ __forceinline__ void fetch_pos(int (&kp)[Tile<R>::L], const HeadDev& hd, int jblk, int S, int tid) {
+#pragma unroll
+  for (int it = 0; it < Tile<R>::L; ++it) kp[it] = slot_pos(hd.kperm, jblk * B + ((tid + it * Tile<R>::NT) >> 4), S);
+}
+
+// Global loads of one K/V block (positions from fetch_pos). Padding slots
+// read key row 0 (always present); their V is zeroed and their scores are
+// masked, so the values never reach the output.
+template <int R>
+__device__ __forceinline__ void fetch_block(BlockRegs<R>& r, const AttnArgs& a, const HeadDev& hd,
+                                            const int (&kp)[Tile<R>::L], int tid) {
   const uint16_t* kb = reinterpret_cast<const uint16_t*>(a.k.p) + (int64_t)hd.kvh * a.k.sh;
   const uint16_t* vb = reinterpret_cast<const uint16_t*>(a.v.p) + (int64_t)hd.kvh * a.v.sh;
 #pragma unroll
   for (int it = 0; it < Tile<R>::L; ++it) {
-    const int u = tid + it * Tile<R>::NT;
-    const int key = u >> 4, chunk = u & 15;
-    const int kp = slot_pos(hd.kperm, jblk * B + key, a.S);
-    const int row = kp >= 0 ? kp : 0;
+    const int chunk = (tid + it * Tile<R>::NT) & 15;
+    const int row = kp[it] >= 0 ? kp[it] : 0;
     r.k[it] = load16(kb + (int64_t)row * a.k.ss + chunk * 8);
     const bf16x8 vv = load16(vb + (int64_t)row * a.v.ss + chunk * 8);
-    r.v[it] = kp >= 0 ? vv : zero8();
+    r.v[it] = kp[it] >= 0 ? vv : zero8();
+    r.kp[it] = kp[it];
   }
 }
 
 template <int R>
-__device__ __forceinline__ void stage_block(Stage& st, const BlockRegs<R>& r, const HeadDev& hd, int jblk, int S,
-                                            int tid) {
+__device__ __forceinline__ void stage_block(Stage& st, const BlockRegs<R>& r, int tid) {
 #pragma unroll
   for (int it = 0; it < Tile<R>::L; ++it) {
     const int u = tid + it * Tile<R>::NT;
     const int key = u >> 4, chunk = u & 15;
     *reinterpret_cast<bf16x8*>(&st.k[key * KPITCH + chunk * 8]) = r.k[it];
     *reinterpret_cast<bf16x8*>(&st.v[key * VPITCH + chunk * 8]) = r.v[it];
-  }
-  if (tid < B) {
-    const int kp = slot_pos(hd.kperm, jblk * B + tid, S);
-    st.kpos[tid] = kp >= 0 ? kp : INT_BIG;
+    if (chunk == 0) st.kpos[key] = r.kp[it] >= 0 ? r.kp[it] : INT_BIG;
   }
 }
 
-// Largest key position of key block j, or INT_BIG if the block holds padding.
-__device__ __forceinline__ int block_kmax(const HeadDev& hd, int j, int S) {
-  if (hd.kmaxpos) return ld_uniform(hd.kmaxpos + j);
-  const int last = j * B + B - 1;
-  return last < S ? last : INT_BIG;
-}
+// Union entries of a work item, read 64 at a time into one VGPR per lane and
+// taken out with readlane (wave-uniform results, no scalar-load waits on the
+// LDS counter inside the block loop).
+struct EntryStream {
+  const int32_t* ent;
+  int n, lane;
+  int cur, nxt;                // entries [base, base+64) and [base+64, base+128)
+  __device__ __forceinline__ void init(const int32_t* e, int count, int ln) {
+    ent = e; n = count; lane = ln;
+    cur = lane < n ? ld_global(ent + lane) : 0;
+    nxt = 64 + lane < n ? ld_global(ent + 64 + lane) : 0;
+  }
+  // entry i; calls come with i = 0, 1, 2, ... in order
+  __device__ __forceinline__ int get(int i) {
+    if (i >= n) return 0;
+    if (i >= 64 && (i & 63) == 0) {
+      cur = nxt;
+      nxt = i + 64 + lane < n ? ld_global(ent + i + 64 + lane) : 0;
+    }
+    return __builtin_amdgcn_readlane(cur, i & 63);
+  }
+};
 
 // Work-item order: hardware hands consecutive workgroups to the 8 XCDs in
 // turn. Runs of XCD_RUN consecutive items go to one XCD, and the runs are
@@ -208,21 +229,25 @@ struct WaveState {
   f32x16 o[4];
   bf16x8 qr[8];
   float m, l;
-  int qpos, qmin, rb, c, h, vlane;
+  int qpos, rb, c, h, vlane;
 };
 
-// One key block t (union entries et .. et3 = entries t .. t+3, 0 past the
-// end). s_cur holds the scores of block t if the wave takes part in it;
-// s_nxt receives those of block t+1. The early half multiplies P(t)V(t)
-// before the barrier that ends the step, the late half right after it.
+// One key block t. et / et1 are the union entries t and t+1 (0 past the
+// end): key block in bits 0-15, member flags from bit 16 (block selected)
+// and from bit 24 (block reaches past the member's first query: mask).
+// s_cur holds the scores of block t if the wave takes part in it; s_nxt
+// receives those of block t+1. On entry `regs` holds block t+2 (loads in
+// flight) and kpn the key positions of block t+3. The early half multiplies
+// P(t)V(t) before the barrier that ends the step, the late half after it.
 template <int R, bool LATE>
 __device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const AttnArgs& a, const HeadDev& hd,
-                                           BlockRegs<R>& regs, int tid, int t, int n, int et, int et1, int et2,
-                                           int et3, f32x16 (&s_cur)[2], f32x16 (&s_nxt)[2], float sc) {
+                                           BlockRegs<R>& regs, int (&kpn)[Tile<R>::L], int tid, int t, int n,
+                                           int et, int et1, int et4, f32x16 (&s_cur)[2], f32x16 (&s_nxt)[2],
+                                           float sc) {
   const int cs = t & (NSTAGE - 1), ns = (t + 1) & (NSTAGE - 1);
   const bool act_c = (et >> (16 + ws.rb)) & 1;
   const bool act_n = t + 1 < n && ((et1 >> (16 + ws.rb)) & 1);
-  if (act_c && block_kmax(hd, et & 0xffff, a.S) > ws.qmin) mask_block(stg[cs], ws.qpos, ws.h, s_cur);
+  if (act_c && ((et >> (24 + ws.rb)) & 1)) mask_block(stg[cs], ws.qpos, ws.h, s_cur);
   float alpha = 1.0f;
   bf16x8 pb[4];
   if (act_c && act_n) {
@@ -240,33 +265,52 @@ __device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const Attn
       for (int x = 0; x < 16; ++x) ws.o[dt][x] *= alpha;
   }
   if (!LATE && act_c) pv_block(stg[cs], pb, ws.vlane, ws.o);
-  // stage t+2 (its stage was last read in step t-1), start loading t+3
-  if (t + 2 < n) stage_block<R>(stg[(t + 2) & (NSTAGE - 1)], regs, hd, et2 & 0xffff, a.S, tid);
-  if (t + 3 < n) fetch_block<R>(regs, a, hd, et3 & 0xffff, tid);
+  // stage t+2 (its stage was last read in step t-1), load t+3, positions of t+4
+  if (t + 2 < n) stage_block<R>(stg[(t + 2) & (NSTAGE - 1)], regs, tid);
+  if (t + 3 < n) fetch_block<R>(regs, a, hd, kpn, tid);
+  if (t + 4 < n) fetch_pos<R>(kpn, hd, et4 & 0xffff, a.S, tid);
   __syncthreads();
   if (LATE && act_c) pv_block(stg[cs], pb, ws.vlane, ws.o);
 }
 
 template <int R, bool LATE>
 __device__ __forceinline__ void block_loop(WaveState& ws, Stage* stg, const AttnArgs& a, const HeadDev& hd,
-                                           const WorkItem& w, BlockRegs<R>& regs, int tid) {
+                                           const WorkItem& w, int tid) {
   const float sc = 0.08838834764831845f * LOG2E;   // sqrt(1/128) * log2(e)
   const int n = w.e1 - w.e0;
-  const int32_t* ent = hd.gcol + w.e0;
-  int e0 = ld_uniform(ent);
-  int e1 = n > 1 ? ld_uniform(ent + 1) : 0;
-  int e2 = n > 2 ? ld_uniform(ent + 2) : 0;
+  EntryStream es;
+  es.init(hd.gcol + w.e0, n, tid & 63);
+  int e0 = es.get(0), e1 = es.get(1), e2 = es.get(2), e3 = es.get(3);
+
+  // prologue: blocks 0 and 1 staged, block 2 loading, positions of block 3
+  BlockRegs<R> regs;
+  int kpn[Tile<R>::L];
+  fetch_pos<R>(kpn, hd, e0 & 0xffff, a.S, tid);
+  fetch_block<R>(regs, a, hd, kpn, tid);
+  stage_block<R>(stg[0], regs, tid);
+  if (n > 1) {
+    fetch_pos<R>(kpn, hd, e1 & 0xffff, a.S, tid);
+    fetch_block<R>(regs, a, hd, kpn, tid);
+    stage_block<R>(stg[1], regs, tid);
+  }
+  if (n > 2) {
+    fetch_pos<R>(kpn, hd, e2 & 0xffff, a.S, tid);
+    fetch_block<R>(regs, a, hd, kpn, tid);
+  }
+  if (n > 3) fetch_pos<R>(kpn, hd, e3 & 0xffff, a.S, tid);
+  __syncthreads();
+
   f32x16 sa[2], sb[2];
   if ((e0 >> (16 + ws.rb)) & 1) qk_block(stg[0], ws.qr, ws.c, ws.h, sa);
   // two steps per trip so that the score buffers swap roles without copies
   for (int t = 0; t < n; t += 2) {
-    int e3 = t + 3 < n ? ld_uniform(ent + t + 3) : 0;
-    block_step<R, LATE>(ws, stg, a, hd, regs, tid, t, n, e0, e1, e2, e3, sa, sb, sc);
-    e0 = e1; e1 = e2; e2 = e3;
+    int e4 = es.get(t + 4);
+    block_step<R, LATE>(ws, stg, a, hd, regs, kpn, tid, t, n, e0, e1, e4, sa, sb, sc);
+    e0 = e1; e1 = e2; e2 = e3; e3 = e4;
     if (t + 1 >= n) break;
-    e3 = t + 4 < n ? ld_uniform(ent + t + 4) : 0;
-    block_step<R, LATE>(ws, stg, a, hd, regs, tid, t + 1, n, e0, e1, e2, e3, sb, sa, sc);
-    e0 = e1; e1 = e2; e2 = e3;
+    e4 = es.get(t + 5);
+    block_step<R, LATE>(ws, stg, a, hd, regs, kpn, tid, t + 1, n, e0, e1, e4, sb, sa, sc);
+    e0 = e1; e1 = e2; e2 = e3; e3 = e4;
   }
 }
 
@@ -289,10 +333,6 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
   ws.h = lane >> 5;
   const int qblk = group_row(w.group, ws.rb, R, hd.gp[0]);
   ws.qpos = qblk < hd.nbq ? slot_pos(hd.qperm, qblk * B + half * 32 + ws.c, a.S) : -1;
-  int qmin = ws.qpos >= 0 ? ws.qpos : INT_BIG;   // smallest valid query position of the wave
-#pragma unroll
-  for (int off = 1; off < 32; off <<= 1) qmin = min(qmin, __shfl_xor(qmin, off));
-  ws.qmin = qmin;
   {
     const uint16_t* qb = reinterpret_cast<const uint16_t*>(a.q.p) + (int64_t)w.head * a.q.sh;
     const uint16_t* row = qb + (int64_t)max(ws.qpos, 0) * a.q.ss + ws.h * 64;
@@ -309,20 +349,8 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
   ws.m = NEG_BIG;
   ws.l = 0.0f;
 
-  // prologue: blocks 0 and 1 staged, block 2 in registers
-  const int n = w.e1 - w.e0;
-  const int32_t* ent = hd.gcol + w.e0;
-  BlockRegs<R> regs;
-  fetch_block<R>(regs, a, hd, ld_uniform(ent) & 0xffff, tid);
-  stage_block<R>(stg[0], regs, hd, ld_uniform(ent) & 0xffff, a.S, tid);
-  if (n > 1) {
-    fetch_block<R>(regs, a, hd, ld_uniform(ent + 1) & 0xffff, tid);
-    stage_block<R>(stg[1], regs, hd, ld_uniform(ent + 1) & 0xffff, a.S, tid);
-  }
-  if (n > 2) fetch_block<R>(regs, a, hd, ld_uniform(ent + 2) & 0xffff, tid);
-  __syncthreads();
-  if (late) block_loop<R, true>(ws, stg, a, hd, w, regs, tid);
-  else block_loop<R, false>(ws, stg, a, hd, w, regs, tid);
+  if (late) block_loop<R, true>(ws, stg, a, hd, w, tid);
+  else block_loop<R, false>(ws, stg, a, hd, w, tid);
 
   const float m = ws.m, l = ws.l;
   const int qpos = ws.qpos, h = ws.h;

@@ -430,16 +430,28 @@ __global__ __launch_bounds__(256) void k_blocks_fill(const HeadDev* heads) {
   }
 }
 
-// Union entries of a row group: key block | (bit r set if query block r of
-// the group selects it) << 16, ascending in the key block.
+// Union entries of a row group, ascending in the key block: key block in
+// bits 0-15, bit 16+r set if query block r of the group selects it, bit 24+r
+// set if it does and the key block holds a position above the smallest
+// query position of query block r (or padding), i.e. needs the causal mask.
 __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R) {
   const HeadDev hd = heads[blockIdx.x];
   const int gr = blockIdx.y;
   if (gr >= hd.gp[1]) return;
   const int rho = hd.gp[0];
   __shared__ int buf[256];
+  __shared__ int qmin[4];
   int rows[4];
   for (int r = 0; r < 4; ++r) rows[r] = r < R ? group_row(gr, r, R, rho) : hd.nbq;
+  // smallest query position of each member (for the mask flags)
+  if (threadIdx.x < 4) qmin[threadIdx.x] = INT_BIG;
+  __syncthreads();
+  for (int x = threadIdx.x; x < R * B; x += blockDim.x) {
+    const int r = x / B, slot = rows[r] * B + x % B;
+    if (rows[r] >= hd.nbq) continue;
+    const int p = hd.qperm ? hd.qperm[slot] : (slot < hd.S ? slot : -1);
+    if (p >= 0) atomicMin(&qmin[r], p);
+  }
   const int per = (hd.nwords + 255) / 256;
   const int w0 = threadIdx.x * per;
   int cnt = 0;
@@ -467,9 +479,17 @@ __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R)
     }
     while (u) {
       const int b = __ffs(u) - 1;
-      int flags = 0;
-      for (int r = 0; r < R; ++r) flags |= ((bits[r] >> b) & 1u) << r;
-      hd.gcol[pos++] = (w * 32 + b) | (flags << 16);
+      const int j = w * 32 + b;
+      int kmax;                      // largest key position of block j, INT_BIG with padding
+      if (hd.kmaxpos) kmax = hd.kmaxpos[j];
+      else kmax = j * B + B - 1 < hd.S ? j * B + B - 1 : INT_BIG;
+      uint32_t flags = 0;
+      for (int r = 0; r < R; ++r) {
+        const uint32_t sel = (bits[r] >> b) & 1u;
+        flags |= sel << (16 + r);
+        if (sel && kmax > qmin[r]) flags |= 1u << (24 + r);
+      }
+      hd.gcol[pos++] = (int32_t)((uint32_t)j | flags);
       u &= u - 1;
     }
   }
