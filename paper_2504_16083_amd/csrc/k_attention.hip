@@ -69,27 +69,57 @@ struct BlockRegs {
   int kp[Tile<R>::L];          // original positions of the thread's keys (-1 = padding)
 };
 
-// Original positions of the keys this thread loads from key block jblk.
+// Per-thread view of the K/V rows it loads. A thread always loads the same
+// 16-byte chunk (tid % 16) of keys key0, key0 + NT/16, ...; K and V of the
+// KV head are buffer resources (base and size in scalar registers), and a
+// row's byte offset is one 24-bit multiply-add: positions are below 2^21
+// and S times the token stride in bytes stays below 2^32 (checked on the
+// host). Loads past the resource size would read zeros.
 template <int R>
-__device__ __forceinline__ void fetch_pos(int (&kp)[Tile<R>::L], const HeadDev& hd, int jblk, int S, int tid) {
+struct KeySrc {
+  __amdgpu_buffer_rsrc_t kr, vr;
+  uint32_t kss, vss;          // token strides in bytes
+  uint32_t cb;                // this thread's chunk offset in bytes
+  const int32_t* perm;
+  int S, key0;
+  __device__ __forceinline__ void init(const AttnArgs& a, const HeadDev& hd, int tid) {
+    const uint16_t* kb = reinterpret_cast<const uint16_t*>(a.k.p) + (int64_t)hd.kvh * a.k.sh;
+    const uint16_t* vb = reinterpret_cast<const uint16_t*>(a.v.p) + (int64_t)hd.kvh * a.v.sh;
+    kss = (uint32_t)a.k.ss * 2u;
+    vss = (uint32_t)a.v.ss * 2u;
+    kr = __builtin_amdgcn_make_buffer_rsrc((void*)kb, (short)0, (int)((uint32_t)(a.S - 1) * kss + 2u * D), 0x00020000);
+    vr = __builtin_amdgcn_make_buffer_rsrc((void*)vb, (short)0, (int)((uint32_t)(a.S - 1) * vss + 2u * D), 0x00020000);
+    cb = (uint32_t)(tid & 15) * 16u;
+    perm = hd.kperm;
+    S = a.S;
+    key0 = tid >> 4;
+  }
+};
+
+__device__ __forceinline__ bf16x8 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+
+// Original positions of the keys this thread loads from key block jblk.
+template <int R, bool PERM>
+__device__ __forceinline__ void fetch_pos(int (&kp)[Tile<R>::L], const KeySrc<R>& ks, int jblk) {
 #pragma unroll
-  for (int it = 0; it < Tile<R>::L; ++it) kp[it] = slot_pos(hd.kperm, jblk * B + ((tid + it * Tile<R>::NT) >> 4), S);
+  for (int it = 0; it < Tile<R>::L; ++it) {
+    const int slot = jblk * B + ks.key0 + it * (Tile<R>::NT / 16);
+    kp[it] = PERM ? ld_global(ks.perm + slot) : (slot < ks.S ? slot : -1);
+  }
 }
 
 // Global loads of one K/V block (positions from fetch_pos). Padding slots
 // read key row 0 (always present); their V is zeroed and their scores are
 // masked, so the values never reach the output.
 template <int R>
-__device__ __forceinline__ void fetch_block(BlockRegs<R>& r, const AttnArgs& a, const HeadDev& hd,
-                                            const int (&kp)[Tile<R>::L], int tid) {
-  const uint16_t* kb = reinterpret_cast<const uint16_t*>(a.k.p) + (int64_t)hd.kvh * a.k.sh;
-  const uint16_t* vb = reinterpret_cast<const uint16_t*>(a.v.p) + (int64_t)hd.kvh * a.v.sh;
+__device__ __forceinline__ void fetch_block(BlockRegs<R>& r, const KeySrc<R>& ks, const int (&kp)[Tile<R>::L]) {
 #pragma unroll
   for (int it = 0; it < Tile<R>::L; ++it) {
-    const int chunk = (tid + it * Tile<R>::NT) & 15;
-    const int row = kp[it] >= 0 ? kp[it] : 0;
-    r.k[it] = load16(kb + (int64_t)row * a.k.ss + chunk * 8);
-    const bf16x8 vv = load16(vb + (int64_t)row * a.v.ss + chunk * 8);
+    const uint32_t row = kp[it] >= 0 ? (uint32_t)kp[it] : 0u;
+    r.k[it] = buffer_load16(ks.kr, __umul24(row, ks.kss) + ks.cb);
+    const bf16x8 vv = buffer_load16(ks.vr, __umul24(row, ks.vss) + ks.cb);
     r.v[it] = kp[it] >= 0 ? vv : zero8();
     r.kp[it] = kp[it];
   }
@@ -172,9 +202,22 @@ __device__ __forceinline__ void mask_block(const Stage& st, int qpos, int h, f32
     }
 }
 
+// Combination of the two 32-lane halves (lanes l and l ^ 32 hold the two
+// halves of a query's scores) by a lane swap instead of an LDS permute.
+__device__ __forceinline__ float xhalf_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float xhalf_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Online-softmax step on the scores of one block: P = 2^(s*sc - m) packed to
-// bf16 B operands, row sum into l. m moves (and alpha < 1 is returned) only
-// when some row's block maximum passes it by more than RESCALE_SLACK.
+// bf16 B operands, row sum into l. m moves (alpha < 1) only when some row's
+// block maximum passes it by more than RESCALE_SLACK. Branch-free, so that
+// the compiler can interleave it with independent MFMAs.
 __device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m, float& l, bf16x8 (&pb)[4],
                                               float& alpha) {
   float mx = NEG_BIG;
@@ -182,19 +225,17 @@ __device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m
   for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
     for (int x = 0; x < 16; ++x) mx = fmaxf(mx, s[kt][x]);
-  mx = fmaxf(mx, __shfl_xor(mx, 32)) * sc;     // scale > 0: max commutes with it
-  alpha = 1.0f;
-  if (__any(mx > m + RESCALE_SLACK)) {
-    const float m_new = fmaxf(m, mx);
-    alpha = fast_exp2(m - m_new);
-    m = m_new;
-  }
+  mx = xhalf_max(mx) * sc;                       // scale > 0: max commutes with it
+  const bool move = __any(mx > m + RESCALE_SLACK);
+  const float m_new = move ? fmaxf(m, mx) : m;
+  alpha = fast_exp2(m - m_new);
+  m = m_new;
   float rs = 0.0f;
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
     for (int x = 0; x < 16; ++x) {
-      const float p = fast_exp2(fmaf(s[kt][x], sc, -m));
+      const float p = fast_exp2(fmaf(s[kt][x], sc, -m_new));
       s[kt][x] = p;
       rs += p;
     }
@@ -204,8 +245,7 @@ __device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m
 #pragma unroll
     for (int x = 0; x < 8; ++x) pb[stp][x] = (__bf16)s[kt][4 * (2 * half + (x >> 2)) + (x & 3)];
   }
-  rs += __shfl_xor(rs, 32);
-  l = l * alpha + rs;
+  l = l * alpha + xhalf_sum(rs);
 }
 
 // O^T += V^T P^T; the V^T operand comes from row-major V by transpose reads.
@@ -232,85 +272,186 @@ struct WaveState {
   int qpos, rb, c, h, vlane;
 };
 
-// One key block t. et / et1 are the union entries t and t+1 (0 past the
-// end): key block in bits 0-15, member flags from bit 16 (block selected)
-// and from bit 24 (block reaches past the member's first query: mask).
-// s_cur holds the scores of block t if the wave takes part in it; s_nxt
-// receives those of block t+1. On entry `regs` holds block t+2 (loads in
-// flight) and kpn the key positions of block t+3. The early half multiplies
-// P(t)V(t) before the barrier that ends the step, the late half after it.
-template <int R, bool LATE>
-__device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const AttnArgs& a, const HeadDev& hd,
-                                           BlockRegs<R>& regs, int (&kpn)[Tile<R>::L], int tid, int t, int n,
-                                           int et, int et1, int et4, f32x16 (&s_cur)[2], f32x16 (&s_nxt)[2],
-                                           float sc) {
-  const int cs = t & (NSTAGE - 1), ns = (t + 1) & (NSTAGE - 1);
-  const bool act_c = (et >> (16 + ws.rb)) & 1;
-  const bool act_n = t + 1 < n && ((et1 >> (16 + ws.rb)) & 1);
-  if (act_c && ((et >> (24 + ws.rb)) & 1)) mask_block(stg[cs], ws.qpos, ws.h, s_cur);
-  float alpha = 1.0f;
-  bf16x8 pb[4];
-  if (act_c && act_n) {
-    // QK MFMAs of block t+1 are independent of the softmax of block t
-    qk_block(stg[ns], ws.qr, ws.c, ws.h, s_nxt);
-    softmax_block(s_cur, sc, ws.m, ws.l, pb, alpha);
+__device__ __forceinline__ bool sel(int e, int rb) { return (e >> (16 + rb)) & 1; }
+__device__ __forceinline__ bool needs_mask(int e, int rb) { return (e >> (24 + rb)) & 1; }
+
+// Softmax of one block cut into pieces that can be spread between MFMAs:
+// 0-3 running maximum over 8 scores each, 4 new maximum, 5-36 one
+// exponential each, 37-40 bf16 packing, 41 row sum.
+constexpr int SM_PIECES = 42;
+
+struct SoftmaxState {
+  float mx, m_new, rs;
+};
+
+__device__ __forceinline__ void softmax_piece(int pc, f32x16 (&s)[2], float sc, float& m, float& l,
+                                              bf16x8 (&pb)[4], float& alpha, SoftmaxState& st) {
+  if (pc < 4) {
+    const int kt = pc >> 1, x0 = (pc & 1) * 8;
+    float v = pc == 0 ? NEG_BIG : st.mx;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) v = fmaxf(v, s[kt][x0 + x]);
+    st.mx = v;
+  } else if (pc == 4) {
+    const float mx = xhalf_max(st.mx) * sc;      // scale > 0: max commutes with it
+    const bool move = __any(mx > m + RESCALE_SLACK);
+    st.m_new = move ? fmaxf(m, mx) : m;
+    alpha = fast_exp2(m - st.m_new);
+    m = st.m_new;
+    st.rs = 0.0f;
+  } else if (pc < 37) {
+    const int e = pc - 5, kt = e >> 4, x = e & 15;
+    const float p = fast_exp2(fmaf(s[kt][x], sc, -st.m_new));
+    s[kt][x] = p;
+    st.rs += p;
+  } else if (pc < 41) {
+    const int stp = pc - 37, kt = stp >> 1, half = stp & 1;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) pb[stp][x] = (__bf16)s[kt][4 * (2 * half + (x >> 2)) + (x & 3)];
   } else {
-    if (act_n) qk_block(stg[ns], ws.qr, ws.c, ws.h, s_nxt);
-    if (act_c) softmax_block(s_cur, sc, ws.m, ws.l, pb, alpha);
+    l = l * alpha + xhalf_sum(st.rs);
   }
-  if (act_c && __any(alpha != 1.0f)) {
+}
+
+// The three pieces of step t that share no data: QK(t+2) and PV(t) on the
+// matrix cores, softmax(t+1) on the vector ALU. They are written out
+// interleaved (MFMA, then a share of the softmax), because the hardware
+// overlaps vector instructions only with MFMAs of the same wave. MFMA A
+// operands are read from LDS three slots ahead.
+template <bool QK, bool PV>
+__device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, const Stage& vst, f32x16 (&s_qk)[2],
+                                           const bf16x8 (&p_cur)[4], f32x16 (&s_sm)[2], bf16x8 (&p_new)[4],
+                                           float sc, float& alpha) {
+  constexpr int NQ = QK ? 16 : 0;
+  constexpr int NM = NQ + (PV ? 16 : 0);
+  constexpr int AHEAD = 3;
+  SoftmaxState st;
+  const f32x16 zero = {};
+  // A operand of MFMA slot i: K rows for QK slots, transposed V for PV slots
+  auto operand = [&](int i) -> bf16x8 {
+    if (i < NQ) {
+      const int st8 = i >> 1, kt = i & 1;
+      return *reinterpret_cast<const bf16x8*>(&kst.k[(kt * 32 + ws.c) * KPITCH + ws.h * 64 + st8 * 8]);
+    }
+    const int j = i - NQ, stp = j >> 2, dt = j & 3, kt = stp >> 1, half = stp & 1;
+    const uint16_t* p0 = &vst.v[ws.vlane + (32 * kt + 16 * half) * VPITCH + 32 * dt];
+    const bf16x4 lo = tr_read(p0);
+    const bf16x4 hi = tr_read(p0 + 8 * VPITCH);
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  };
+  bf16x8 opa[AHEAD + 1];
+#pragma unroll
+  for (int i = 0; i < AHEAD && i < NM; ++i) opa[i] = operand(i);
+  int pc = 0;
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    if (i + AHEAD < NM) opa[(i + AHEAD) % (AHEAD + 1)] = operand(i + AHEAD);
+    const bf16x8 av = opa[i % (AHEAD + 1)];
+    if (i < NQ) {
+      const int st8 = i >> 1, kt = i & 1;
+      s_qk[kt] = mfma32(av, ws.qr[st8], st8 == 0 ? zero : s_qk[kt]);
+    } else {
+      const int j = i - NQ, stp = j >> 2, dt = j & 3;
+      ws.o[dt] = mfma32(av, p_cur[stp], ws.o[dt]);
+    }
+    const int pe = (i + 1) * SM_PIECES / NM;
+#pragma unroll
+    for (; pc < pe; ++pc) softmax_piece(pc, s_sm, sc, ws.m, ws.l, p_new, alpha, st);
+  }
+#pragma unroll
+  for (; pc < SM_PIECES; ++pc) softmax_piece(pc, s_sm, sc, ws.m, ws.l, p_new, alpha, st);
+}
+
+// Step t. Entries e0..e2 are the union entries t..t+2 (0 past the end): key
+// block in bits 0-15, per-member select flags from bit 16, per-member mask
+// flags from bit 24. On entry: P(t) in p_cur, the scores of block t+1 in
+// s_sm, `regs` loading block t+3, kpn the key positions of block t+4. The
+// step multiplies P(t)V(t), turns the scores of t+1 into P(t+1) (p_new),
+// computes the scores of t+2 into s_qk, stages t+3 and starts loading t+4.
+template <int R, bool PERM>
+__device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const KeySrc<R>& ks,
+                                           BlockRegs<R>& regs, int (&kpn)[Tile<R>::L], int tid, int t, int n,
+                                           int e0, int e1, int e2, int e5, f32x16 (&s_qk)[2],
+                                           const bf16x8 (&p_cur)[4], f32x16 (&s_sm)[2], bf16x8 (&p_new)[4],
+                                           float sc) {
+  const bool a0 = sel(e0, ws.rb);
+  const bool a1 = t + 1 < n && sel(e1, ws.rb);
+  const bool a2 = t + 2 < n && sel(e2, ws.rb);
+  const Stage& vst = stg[t & (NSTAGE - 1)];
+  const Stage& kst = stg[(t + 2) & (NSTAGE - 1)];
+  float alpha = 1.0f;
+  if (a1) {
+    if (needs_mask(e1, ws.rb)) mask_block(stg[(t + 1) & (NSTAGE - 1)], ws.qpos, ws.h, s_sm);
+    if (a2 && a0) fused_step<true, true>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    else if (a2) fused_step<true, false>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    else if (a0) fused_step<false, true>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    else fused_step<false, false>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+  } else {
+    if (a2) qk_block(kst, ws.qr, ws.c, ws.h, s_qk);
+    if (a0) pv_block(vst, p_cur, ws.vlane, ws.o);
+  }
+  // stage t+3 (its stage was last read in step t-1), load t+4, positions of t+5
+  if (t + 3 < n) stage_block<R>(stg[(t + 3) & (NSTAGE - 1)], regs, tid);
+  if (t + 4 < n) fetch_block<R>(regs, ks, kpn);
+  if (t + 5 < n) fetch_pos<R, PERM>(kpn, ks, e5 & 0xffff);
+  // O holds P(t)V(t) relative to the old maximum: move it to the new one
+  if (a1 && __any(alpha != 1.0f)) {
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int x = 0; x < 16; ++x) ws.o[dt][x] *= alpha;
   }
-  if (!LATE && act_c) pv_block(stg[cs], pb, ws.vlane, ws.o);
-  // stage t+2 (its stage was last read in step t-1), load t+3, positions of t+4
-  if (t + 2 < n) stage_block<R>(stg[(t + 2) & (NSTAGE - 1)], regs, tid);
-  if (t + 3 < n) fetch_block<R>(regs, a, hd, kpn, tid);
-  if (t + 4 < n) fetch_pos<R>(kpn, hd, et4 & 0xffff, a.S, tid);
   __syncthreads();
-  if (LATE && act_c) pv_block(stg[cs], pb, ws.vlane, ws.o);
 }
 
-template <int R, bool LATE>
+template <int R, bool PERM>
 __device__ __forceinline__ void block_loop(WaveState& ws, Stage* stg, const AttnArgs& a, const HeadDev& hd,
                                            const WorkItem& w, int tid) {
+  KeySrc<R> ks;
+  ks.init(a, hd, tid);
   const float sc = 0.08838834764831845f * LOG2E;   // sqrt(1/128) * log2(e)
   const int n = w.e1 - w.e0;
   EntryStream es;
   es.init(hd.gcol + w.e0, n, tid & 63);
-  int e0 = es.get(0), e1 = es.get(1), e2 = es.get(2), e3 = es.get(3);
+  int e0 = es.get(0), e1 = es.get(1), e2 = es.get(2), e3 = es.get(3), e4 = es.get(4);
 
-  // prologue: blocks 0 and 1 staged, block 2 loading, positions of block 3
+  // prologue: blocks 0-2 staged, block 3 loading, positions of block 4
   BlockRegs<R> regs;
   int kpn[Tile<R>::L];
-  fetch_pos<R>(kpn, hd, e0 & 0xffff, a.S, tid);
-  fetch_block<R>(regs, a, hd, kpn, tid);
-  stage_block<R>(stg[0], regs, tid);
-  if (n > 1) {
-    fetch_pos<R>(kpn, hd, e1 & 0xffff, a.S, tid);
-    fetch_block<R>(regs, a, hd, kpn, tid);
-    stage_block<R>(stg[1], regs, tid);
+  const int ep[3] = {e0, e1, e2};
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    if (j < n) {
+      fetch_pos<R, PERM>(kpn, ks, ep[j] & 0xffff);
+      fetch_block<R>(regs, ks, kpn);
+      stage_block<R>(stg[j], regs, tid);
+    }
   }
-  if (n > 2) {
-    fetch_pos<R>(kpn, hd, e2 & 0xffff, a.S, tid);
-    fetch_block<R>(regs, a, hd, kpn, tid);
+  if (n > 3) {
+    fetch_pos<R, PERM>(kpn, ks, e3 & 0xffff);
+    fetch_block<R>(regs, ks, kpn);
   }
-  if (n > 3) fetch_pos<R>(kpn, hd, e3 & 0xffff, a.S, tid);
+  if (n > 4) fetch_pos<R, PERM>(kpn, ks, e4 & 0xffff);
   __syncthreads();
 
   f32x16 sa[2], sb[2];
-  if ((e0 >> (16 + ws.rb)) & 1) qk_block(stg[0], ws.qr, ws.c, ws.h, sa);
-  // two steps per trip so that the score buffers swap roles without copies
+  bf16x8 pa[4], pb[4];
+  if (sel(e0, ws.rb)) {
+    qk_block(stg[0], ws.qr, ws.c, ws.h, sa);
+    if (needs_mask(e0, ws.rb)) mask_block(stg[0], ws.qpos, ws.h, sa);
+    float alpha;
+    softmax_block(sa, sc, ws.m, ws.l, pa, alpha);
+  }
+  if (n > 1 && sel(e1, ws.rb)) qk_block(stg[1], ws.qr, ws.c, ws.h, sb);
+  // two steps per trip so that the buffers swap roles without copies
   for (int t = 0; t < n; t += 2) {
-    int e4 = es.get(t + 4);
-    block_step<R, LATE>(ws, stg, a, hd, regs, kpn, tid, t, n, e0, e1, e4, sa, sb, sc);
-    e0 = e1; e1 = e2; e2 = e3; e3 = e4;
+    int e5 = es.get(t + 5);
+    block_step<R, PERM>(ws, stg, ks, regs, kpn, tid, t, n, e0, e1, e2, e5, sa, pa, sb, pb, sc);
+    e0 = e1; e1 = e2; e2 = e3; e3 = e4; e4 = e5;
     if (t + 1 >= n) break;
-    e4 = es.get(t + 5);
-    block_step<R, LATE>(ws, stg, a, hd, regs, kpn, tid, t + 1, n, e0, e1, e4, sb, sa, sc);
-    e0 = e1; e1 = e2; e2 = e3; e3 = e4;
+    e5 = es.get(t + 6);
+    block_step<R, PERM>(ws, stg, ks, regs, kpn, tid, t + 1, n, e0, e1, e2, e5, sb, pb, sa, pa, sc);
+    e0 = e1; e1 = e2; e2 = e3; e3 = e4; e4 = e5;
   }
 }
 
@@ -325,10 +466,10 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
   // Waves 0..R-1 own rows 0-31 of member `wave`; waves R..2R-1 own rows
   // 32-63 of member (wave - R + R/2) mod R, so that the two waves sharing a
   // SIMD (wave and wave + 4 for R = 4) serve different members.
-  const bool late = wave >= R;
+  const bool upper = wave >= R;
   WaveState ws;
-  ws.rb = late ? (wave - R + R / 2) % R : wave;
-  const int half = late ? 1 : 0;
+  ws.rb = upper ? (wave - R + R / 2) % R : wave;
+  const int half = upper ? 1 : 0;
   ws.c = lane & 31;
   ws.h = lane >> 5;
   const int qblk = group_row(w.group, ws.rb, R, hd.gp[0]);
@@ -348,8 +489,7 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
     for (int e = 0; e < 16; ++e) ws.o[dt][e] = 0.0f;
   ws.m = NEG_BIG;
   ws.l = 0.0f;
-
-  if (late) block_loop<R, true>(ws, stg, a, hd, w, tid);
+  if (hd.kperm) block_loop<R, true>(ws, stg, a, hd, w, tid);
   else block_loop<R, false>(ws, stg, a, hd, w, tid);
 
   const float m = ws.m, l = ws.l;
