@@ -111,16 +111,16 @@ __device__ __forceinline__ void fetch_pos(int (&kp)[Tile<R>::L], const KeySrc<R>
 }
 
 // Global loads of one K/V block (positions from fetch_pos). Padding slots
-// read key row 0 (always present); their V is zeroed and their scores are
-// masked, so the values never reach the output.
+// read key row 0 (always present); their V is zeroed when staged and their
+// scores are masked, so the values never reach the output. Nothing here
+// touches the loaded data: the loads stay in flight until stage_block.
 template <int R>
 __device__ __forceinline__ void fetch_block(BlockRegs<R>& r, const KeySrc<R>& ks, const int (&kp)[Tile<R>::L]) {
 #pragma unroll
   for (int it = 0; it < Tile<R>::L; ++it) {
     const uint32_t row = kp[it] >= 0 ? (uint32_t)kp[it] : 0u;
     r.k[it] = buffer_load16(ks.kr, __umul24(row, ks.kss) + ks.cb);
-    const bf16x8 vv = buffer_load16(ks.vr, __umul24(row, ks.vss) + ks.cb);
-    r.v[it] = kp[it] >= 0 ? vv : zero8();
+    r.v[it] = buffer_load16(ks.vr, __umul24(row, ks.vss) + ks.cb);
     r.kp[it] = kp[it];
   }
 }
@@ -131,9 +131,10 @@ __device__ __forceinline__ void stage_block(Stage& st, const BlockRegs<R>& r, in
   for (int it = 0; it < Tile<R>::L; ++it) {
     const int u = tid + it * Tile<R>::NT;
     const int key = u >> 4, chunk = u & 15;
+    const bool pad = r.kp[it] < 0;
     *reinterpret_cast<bf16x8*>(&st.k[key * KPITCH + chunk * 8]) = r.k[it];
-    *reinterpret_cast<bf16x8*>(&st.v[key * VPITCH + chunk * 8]) = r.v[it];
-    if (chunk == 0) st.kpos[key] = r.kp[it] >= 0 ? r.kp[it] : INT_BIG;
+    *reinterpret_cast<bf16x8*>(&st.v[key * VPITCH + chunk * 8]) = pad ? zero8() : r.v[it];
+    if (chunk == 0) st.kpos[key] = pad ? INT_BIG : r.kp[it];
   }
 }
 
