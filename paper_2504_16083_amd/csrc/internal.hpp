@@ -177,7 +177,6 @@ struct AttnArgs {
   float* part_o;              // [nparts][R*64][128]
   float* part_ml;             // [nparts][R*64][2]
   int32_t R;                  // query blocks per row group (1, 2 or 4)
-  int32_t wide;               // 1: one wave per query block (64 rows), 0: two waves of 32 rows
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
 hipError_t launch_combine(const AttnArgs& a, const SplitRow* splits, int64_t nsplit, hipStream_t st);

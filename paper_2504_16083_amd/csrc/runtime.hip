@@ -102,7 +102,6 @@ struct mmi_ctx {
   int chunk_blocks = 64;           // smallest work-item length (union entries)
   int items_per_layer = 8192;      // target number of work items per layer
   int row_group = 4;               // query blocks per attention work item (1, 2 or 4)
-  int wide = 0;                    // attention waves own 64 query rows (1) or 32 (0)
   int live_plans = 0;              // plans created from this context and not destroyed
   mmi::Allocator alloc;
   int64_t* pinned = nullptr;       // host staging for totals
@@ -728,7 +727,6 @@ static void plan_execute_impl(mmi_plan* P, const void* q, const void* k, const v
   a.part_o = P->d_part_o;
   a.part_ml = P->d_part_ml;
   a.R = P->R;
-  a.wide = P->ctx->wide;
   HIPCHK(hipEventRecord(P->ev[4], st));
   HIPCHK(launch_attention(a, st));
   HIPCHK(hipEventRecord(P->ev[5], st));
@@ -804,7 +802,6 @@ int mmi_ctx_create(int device, mmi_ctx** out) {
       const int v = atoi(e);
       if (v == 1 || v == 2 || v == 4) c->row_group = v;
     }
-    if (const char* e = getenv("MMI_ATTN_WIDE")) c->wide = atoi(e) != 0;
     *out = c;
   });
 }
