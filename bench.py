@@ -28,6 +28,27 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 FLOP_PER_BLOCK = 4 * 64 * 64 * 128
 
+# HBM traffic of one k_attention launch on the 1M workload, from two rocprofv3
+# --pmc passes (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) scaled by what
+# the same counters read for a plain 1 GiB copy (read x1.939, write x1.000).
+# Keyed by the kernel source's SHA-256 prefix: once the kernel changes the
+# counters are stale and `traffic` is reported as null.
+TRAFFIC = {
+    "840d255ddc9cffb5": {"workload": "cfg4_mm_1m", "fetch_kib": 1452476230, "write_kib": 8523832,
+                         "fetch_scale": 1.939, "write_scale": 1.000},
+}
+
+
+def attention_traffic(workload: str):
+    import hashlib
+    src = os.path.join(ROOT, "paper_2504_16083_amd", "csrc", "k_attention.hip")
+    with open(src, "rb") as f:
+        key = hashlib.sha256(f.read()).hexdigest()[:16]
+    t = TRAFFIC.get(key)
+    if t is None or t["workload"] != workload:
+        return None
+    return (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024.0
+
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
@@ -199,7 +220,7 @@ def main():
                    "density": blocks / causal_blocks, "computed_per_load": blocks / max(loaded, 1)},
         "roofline": {"bound": "mfma", "kernel": "k_attention", "achieved": attn_tflops,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": attn_tflops / PEAK_BF16_TFLOPS,
-                     "traffic": None},
+                     "traffic": attention_traffic(wl.name)},
         "dense": dense,
         "speedup_vs_dense": None if dense is None else dense["speedup_sparse_vs_dense"],
         "cpu_baseline": cpu,
