@@ -973,6 +973,14 @@ int mmi_plan_export(mmi_plan* P, int head, int what, int slot, void* dst, size_t
         }
         break;
       }
+      case MMI_EXPORT_UNION_PTR:
+      case MMI_EXPORT_UNION: {
+        int32_t gp[2];
+        HIPCHK(hipMemcpy(gp, hd.gp, sizeof gp, hipMemcpyDeviceToHost));
+        if (what == MMI_EXPORT_UNION_PTR) { src = hd.growptr; n = (size_t)(gp[1] + 1) * 4; }
+        else { src = hd.gcol; n = (size_t)H.gnnz * 4; }
+        break;
+      }
       default: fail(MMI_ERR_INVALID_ARG, "unknown export kind %d", what);
     }
     if (needed) *needed = n;

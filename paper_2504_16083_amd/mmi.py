@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(HERE, "libmmi.so")
 
 MAXM = 8
 OK = 0
-EXPORT = dict(qperm=0, kperm=1, row_ptr=2, col_idx=3, v=4, u=5, fold=6, vsel=7, ssel=8, params=9, est_lse=10)
+EXPORT = dict(qperm=0, kperm=1, row_ptr=2, col_idx=3, v=4, u=5, fold=6, vsel=7, ssel=8, params=9, est_lse=10,
+              union_ptr=11, union=12)
 _F32 = {"v", "u", "fold", "est_lse"}
 
 

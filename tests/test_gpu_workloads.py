@@ -91,3 +91,50 @@ def test_row_group_stride_choice(ctx):
     rows = np.unique(np.concatenate([np.arange(S - 64, S), np.random.default_rng(1).choice(S, 256, replace=False)]))
     rep = full_check(ctx, S, 2, 1, None, heads, q, k, v, rows=rows)
     say(f"  ties={rep.ties} max|dO|={rep.max_o:.3g}")
+
+
+def expected_union(rp, col, qperm, kperm, S, R, rho, ngroups):
+    """Row-group unions rebuilt from the exported CSR and permutations: per
+    group, ascending key blocks with select bit r (member r lists the block)
+    and mask bit r (member r lists it and its largest key position, INT_BIG
+    with padding, exceeds member r's smallest query position)."""
+    BIG = 0x3FFFFFFF
+    nbq = len(rp) - 1
+    kp = kperm.reshape(-1, 64)
+    kmax = np.where((kp < 0).any(axis=1), BIG, kp.max(axis=1))
+    qp = qperm.reshape(-1, 64)
+    qmin = np.where(qp >= 0, qp, BIG).min(axis=1)
+    ptr, ent = [0], []
+    for g in range(ngroups):
+        rows = [(g // rho) * (R * rho) + g % rho + r * rho for r in range(R)]
+        lists = [set(col[rp[i]:rp[i + 1]].tolist()) if i < nbq else set() for i in rows]
+        for j in sorted(set().union(*lists)):
+            sel = sum(1 << r for r in range(R) if j in lists[r])
+            msk = sum(1 << r for r in range(R) if j in lists[r] and kmax[j] > qmin[rows[r]])
+            ent.append(np.uint32(j | (sel << 16) | (msk << 24)).view(np.int32))
+        ptr.append(len(ent))
+    return np.array(ptr, dtype=np.int32), np.array(ent, dtype=np.int32)
+
+
+def test_row_group_unions(ctx):
+    """The attention work list: every head's row-group union entries, select
+    flags and causal-mask flags, bit-exact against a rebuild from the exported
+    block index and permutations (128K workload, all four head kinds)."""
+    import os
+    from paper_2504_16083_amd import mmi
+    wl = workloads.by_id(2)
+    R = int(os.environ.get("MMI_ROW_GROUP", "4"))
+    q, k, v = generate.make_qkv(wl, "cuda")
+    plan = mmi.Plan(ctx, mmi.Problem(wl.S, wl.Hq, wl.Hkv, wl.modality), wl.heads, q, k)
+    try:
+        for h in range(4):
+            st = plan.stats(h)
+            uptr, uent = plan.export(h, "union_ptr"), plan.export(h, "union")
+            ptr, ent = expected_union(plan.export(h, "row_ptr"), plan.export(h, "col_idx"), plan.export(h, "qperm"),
+                                      plan.export(h, "kperm"), wl.S, R, st.group_stride, len(uptr) - 1)
+            say(f"  head {h}: stride {st.group_stride}, {len(uptr) - 1} groups, {len(uent)} entries")
+            assert len(uent) == st.loaded_blocks
+            np.testing.assert_array_equal(uptr, ptr)
+            np.testing.assert_array_equal(uent, ent)
+    finally:
+        plan.destroy()
