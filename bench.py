@@ -64,6 +64,10 @@ def parse():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8)
+    ap.add_argument("--pattern", default="method",
+                    choices=["method", "ashape", "trishape", "sf_fixed", "sf_strided", "vslash"],
+                    help="every head on one of the paper's baseline patterns (Section 4.1, baseline "
+                         "hyperparameter table) instead of the workload's per-head patterns")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain copy of this many MiB (k_permute, identity) before the steps, "
                          "as the reference dispatch for HBM byte counters")
@@ -128,6 +132,14 @@ def main():
     from synth import generate, workloads
 
     wl = workloads.by_id(args.config)
+    if args.pattern != "method":
+        from synth import config as C
+        tpf = wl.frame or 256        # tokens per frame
+        op = {"ashape": C.ashape(128, 4096), "trishape": C.trishape(128, 4096, 128),
+              "sf_fixed": C.sf_fixed(tpf, tpf), "sf_strided": C.sf_strided(tpf, tpf),
+              "vslash": C.vslash(1000, 1024)}[args.pattern]
+        wl.heads = [C.global_head(op)] * wl.Hq
+        wl.name = f"{wl.name}+{args.pattern}"
     torch.cuda.set_device(0)
     log(f"workload {wl.name}: S={wl.S} Hq={wl.Hq} Hkv={wl.Hkv}")
     q, k, v = generate.make_qkv(wl, "cuda")

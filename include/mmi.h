@@ -71,6 +71,15 @@ extern "C" {
 #define MMI_OP_VERT 5    /* k in the top-n_vertical key columns of the key modality, */
                          /* estimated from the query modality's final queries        */
                          /* (2D-Boundary cross pairs only)                            */
+/* Static baseline patterns (Section 4.1 "Baselines"; Appendix, table of baseline
+ * hyperparameters). No estimation; same coordinates as ASHAPE. */
+#define MMI_OP_SF_FIXED 6    /* Sparse Transformer, fixed: floor(q/local) == floor(k/local) */
+                             /* (same segment) or k = 0 (mod stride_lo) (segment heads)     */
+#define MMI_OP_SF_STRIDED 7  /* Sparse Transformer, strided: q - k < local or              */
+                             /* q - k = 0 (mod stride_lo)                                   */
+#define MMI_OP_TRISHAPE 8    /* A-shape plus every key for the final `bottom` queries:     */
+                             /* k < sink or q - k < local or q >= L - bottom (L = extent   */
+                             /* of the op's coordinates: S, or the modality's length)      */
 
 /* Head kinds. */
 #define MMI_HEAD_GLOBAL 0     /* one op over all rows: No-Boundary / K-Boundary (Sec. 3.2) */
@@ -83,14 +92,17 @@ typedef struct mmi_op {
   int32_t n_vertical, n_slash;   /* VSLASH (both), VERT (n_vertical); >= 0 */
   int32_t stride_lo, stride_hi;  /* GRID: 1 <= lo <= hi <= MMI_MAX_STRIDE */
   int32_t use_h, use_v, use_s;   /* GRID line flags (0/1) */
+  int32_t bottom;                /* TRISHAPE: final queries with full attention, >= 0 */
 } mmi_op;
 
 typedef struct mmi_head_cfg {
   int32_t kind;                  /* MMI_HEAD_* */
-  mmi_op global;                 /* HEAD_GLOBAL: DENSE, ASHAPE, VSLASH or GRID */
+  mmi_op global;                 /* HEAD_GLOBAL: DENSE, ASHAPE, VSLASH, GRID or a static baseline */
   mmi_op intra[MMI_MAX_MODALITIES];
-  /* QBOUNDARY: intra[m] in DENSE, ASHAPE, VSLASH (global positions).
-   * 2D: intra[m] in DENSE, ASHAPE, VSLASH, GRID (modality-local coordinates). */
+  /* QBOUNDARY: intra[m] in DENSE, ASHAPE, VSLASH or a static baseline (global positions).
+   * 2D: intra[m] in DENSE, ASHAPE, VSLASH, GRID or a static baseline (modality-local
+   * coordinates). Static baselines: SF_FIXED, SF_STRIDED (local >= 1, stride_lo >= 1),
+   * TRISHAPE (sink, local, bottom >= 0). */
   mmi_op cross[MMI_MAX_MODALITIES][MMI_MAX_MODALITIES];
   /* 2D: cross[mq][mk], mq != mk, in NONE, DENSE, VERT. */
 } mmi_head_cfg;

@@ -14,7 +14,8 @@ keeps its own key). Every causal element inside a selected block is computed.
 Head kinds (Sections 3.1-3.2):
   * global op (No-Boundary / K-Boundary heads, applied to all rows):
     dense, A-shape, Vertical-Slash (identity order) or Grid (Algorithm 1:
-    permuted by phase);
+    permuted by phase), or one of the static baselines of Section 4.1
+    (Sparse Transformer fixed / strided, Tri-shape; identity order);
   * Q-Boundary (Algorithm 2): queries grouped by modality (each group padded
     to a multiple of B), keys in original order; each modality's queries use
     their own op in global positions, estimated from that modality's final
@@ -159,8 +160,8 @@ def choose(cfg: C.HeadCfg, S: int, modality, q_rows, K: np.ndarray, scale=None):
     if cfg.kind == C.HEAD_QBOUNDARY:
         for m in mods:
             op = cfg.intra_op(m)
-            if op.kind not in (C.OP_DENSE, C.OP_ASHAPE, C.OP_VSLASH):
-                raise NotImplementedError("Q-Boundary intra op must be dense, A-shape or VS")
+            if op.kind not in C.STATIC_OPS + (C.OP_VSLASH,):
+                raise NotImplementedError("Q-Boundary intra op must be VS or a static pattern")
             e = None
             if op.kind == C.OP_VSLASH:
                 rows = layout.final_run_rows(T[m])
@@ -170,8 +171,8 @@ def choose(cfg: C.HeadCfg, S: int, modality, q_rows, K: np.ndarray, scale=None):
     if cfg.kind == C.HEAD_2D:
         for m in mods:
             op = cfg.intra_op(m)
-            if op.kind not in (C.OP_DENSE, C.OP_ASHAPE, C.OP_VSLASH, C.OP_GRID):
-                raise NotImplementedError("2D intra op must be dense, A-shape, VS or Grid")
+            if op.kind not in C.STATIC_OPS + (C.OP_VSLASH, C.OP_GRID):
+                raise NotImplementedError("2D intra op must be VS, Grid or a static pattern")
             Tm = T[m]
             e = None
             if op.kind in (C.OP_GRID, C.OP_VSLASH):
@@ -262,15 +263,28 @@ def _identity_op_blocks(st: OpState, runs, kbase: int):
     at key slot kbase*B + coordinate. runs: row coordinates as [(a, b)]."""
     qmax = runs[-1][1]
     out = set()
-    if st.kind == C.OP_DENSE:
+    if st.kind == C.OP_DENSE or (st.kind == C.OP_TRISHAPE and qmax >= st.L - st.op.bottom):
         out.update(range(0, blk(qmax) + 1))
-    elif st.kind == C.OP_ASHAPE:
+    elif st.kind in (C.OP_ASHAPE, C.OP_TRISHAPE):
         sink, local = st.op.sink, st.op.local
         if sink > 0:
             out.update(range(0, blk(min(sink - 1, qmax)) + 1))
         if local > 0:
             for a, b in runs:
                 out.update(range(blk(max(0, a - local + 1)), blk(b) + 1))
+    elif st.kind == C.OP_SF_FIXED:
+        seg, stride = st.op.local, st.op.stride_lo
+        for a, b in runs:                         # own segment, causal part
+            out.update(range(blk(a // seg * seg), blk(b) + 1))
+        out.update(blk(np.arange(0, qmax + 1, stride)).tolist())   # segment heads
+    elif st.kind == C.OP_SF_STRIDED:
+        local, stride = st.op.local, st.op.stride_lo
+        for a, b in runs:
+            out.update(range(blk(max(0, a - local + 1)), blk(b) + 1))
+            m = np.arange(0, b // stride + 1)
+            lo, hi = blk(np.maximum(0, a - m * stride)), blk(b - m * stride)
+            for x, y in zip(lo.tolist(), hi.tolist()):
+                out.update(range(x, y + 1))
     elif st.kind == C.OP_VSLASH:
         out.update(blk(st.vsel[st.vsel <= qmax]).tolist())
         for a, b in runs:
@@ -404,6 +418,12 @@ def _op_pred(st: OpState, qc, kc):
         return np.zeros(np.broadcast(qc, kc).shape, dtype=bool)
     if st.kind == C.OP_ASHAPE:
         return (kc < st.op.sink) | ((qc - kc) < st.op.local)
+    if st.kind == C.OP_TRISHAPE:
+        return (kc < st.op.sink) | ((qc - kc) < st.op.local) | (qc >= st.L - st.op.bottom)
+    if st.kind == C.OP_SF_FIXED:
+        return ((qc // st.op.local) == (kc // st.op.local)) | (kc % st.op.stride_lo == 0)
+    if st.kind == C.OP_SF_STRIDED:
+        return ((qc - kc) < st.op.local) | ((qc - kc) % st.op.stride_lo == 0)
     if st.kind == C.OP_VSLASH:
         return np.isin(kc, st.vsel) | np.isin(qc - kc, st.ssel)
     if st.kind == C.OP_VERT:

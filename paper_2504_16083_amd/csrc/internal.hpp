@@ -69,6 +69,7 @@ struct OpDev {
   int32_t kind;               // MMI_OP_* (GRID may fall back to dense via params)
   int32_t sink, local;
   int32_t use_h, use_v, use_s;
+  int32_t stride, bottom;     // SF_FIXED / SF_STRIDED stride; TRISHAPE final queries
   int32_t L;                  // extent of the op's coordinate system
   int32_t kbase, nkblk;       // first key block / number of key blocks of the key group
   const int32_t* params;      // GRID: {sigma, phase}

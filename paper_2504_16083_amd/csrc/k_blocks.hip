@@ -99,16 +99,36 @@ __device__ __forceinline__ void set_threshold(uint32_t* bm, const int32_t* thr, 
   }
 }
 
-// dense / A-shape / VS over coordinates whose keys sit at key block kbase + c / 64
+// dense / A-shape / VS / static baselines over coordinates whose keys sit at
+// key block kbase + c / 64 (row coordinates as runs [ra, rb])
 __device__ void identity_rules(uint32_t* bm, const OpDev& op, const int* ra, const int* rb, int nruns,
                                int maxpos, int kbase) {
   const int qmax = rb[nruns - 1];
-  if (op.kind == MMI_OP_DENSE || (op.kind == MMI_OP_GRID)) {   // GRID here = dense fallback
+  if (op.kind == MMI_OP_DENSE || (op.kind == MMI_OP_GRID) ||    // GRID here = dense fallback
+      (op.kind == MMI_OP_TRISHAPE && qmax >= op.L - op.bottom)) {  // a final query sees every key
     set_range(bm, kbase, kbase + qmax / B);
-  } else if (op.kind == MMI_OP_ASHAPE) {
+  } else if (op.kind == MMI_OP_ASHAPE || op.kind == MMI_OP_TRISHAPE) {
     if (op.sink > 0) set_range(bm, kbase, kbase + min(op.sink - 1, qmax) / B);
     if (op.local > 0)
       for (int r = 0; r < nruns; ++r) set_range(bm, kbase + max(0, ra[r] - op.local + 1) / B, kbase + rb[r] / B);
+  } else if (op.kind == MMI_OP_SF_FIXED) {
+    // own segment: keys [floor(q/l) l, q] over the run's rows
+    for (int r = 0; r < nruns; ++r) set_range(bm, kbase + ra[r] / op.local * op.local / B, kbase + rb[r] / B);
+    // segment heads: keys at multiples of the stride up to the last row
+    for (int m = threadIdx.x; m <= qmax / op.stride; m += blockDim.x) set_bit(bm, kbase + m * op.stride / B);
+  } else if (op.kind == MMI_OP_SF_STRIDED) {
+    for (int r = 0; r < nruns; ++r) {
+      set_range(bm, kbase + max(0, ra[r] - op.local + 1) / B, kbase + rb[r] / B);
+      if (rb[r] - ra[r] + 1 >= op.stride) {
+        set_range(bm, kbase, kbase + rb[r] / B);     // the run covers every residue mod stride
+      } else {
+        // keys q - m*stride for the run's rows q: [ra - m s, rb - m s] for every m
+        for (int m = threadIdx.x; m <= rb[r] / op.stride; m += blockDim.x) {
+          const int lo = max(0, ra[r] - m * op.stride) / B, hi = (rb[r] - m * op.stride) / B;
+          for (int j = lo; j <= hi; ++j) set_bit(bm, kbase + j);
+        }
+      }
+    }
   } else if (op.kind == MMI_OP_VSLASH) {
     set_threshold(bm, op.minsel, kbase, op.nkblk, maxpos, false);
     for (int idx = threadIdx.x; idx < op.ns; idx += blockDim.x) {

@@ -209,6 +209,10 @@ static void check_op(const mmi_op& op, std::initializer_list<int> allowed, const
       (op.stride_lo < 1 || op.stride_hi < op.stride_lo || op.stride_hi > MMI_MAX_STRIDE))
     fail(MMI_ERR_BAD_CONFIG, "head %d: grid stride range [%d, %d] outside [1, %d]", h, op.stride_lo,
          op.stride_hi, MMI_MAX_STRIDE);
+  if ((op.kind == MMI_OP_SF_FIXED || op.kind == MMI_OP_SF_STRIDED) && (op.local < 1 || op.stride_lo < 1))
+    fail(MMI_ERR_BAD_CONFIG, "head %d: Sparse Transformer local and stride must be >= 1", h);
+  if (op.kind == MMI_OP_TRISHAPE && (op.sink < 0 || op.local < 0 || op.bottom < 0))
+    fail(MMI_ERR_BAD_CONFIG, "head %d: Tri-shape sink/local/bottom must be >= 0", h);
 }
 
 static void aligned16(const void* p, const char* name) {
@@ -392,16 +396,18 @@ static void validate_cfgs(const Groups& g, const mmi_problem& p, const mmi_head_
   for (int h = 0; h < p.Hq; ++h) {
     const mmi_head_cfg& c = cfgs[h];
     if (c.kind == MMI_HEAD_GLOBAL) {
-      check_op(c.global, {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH, MMI_OP_GRID}, "a global head", h);
+      check_op(c.global, {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH, MMI_OP_GRID, MMI_OP_SF_FIXED,
+                          MMI_OP_SF_STRIDED, MMI_OP_TRISHAPE}, "a global head", h);
     } else if (c.kind == MMI_HEAD_QBOUNDARY) {
       for (int gi = 0; gi < g.n; ++gi)
-        check_op(c.intra[g.mod[gi]], {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH}, "a Q-Boundary modality", h);
+        check_op(c.intra[g.mod[gi]], {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH, MMI_OP_SF_FIXED, MMI_OP_SF_STRIDED,
+                                      MMI_OP_TRISHAPE}, "a Q-Boundary modality", h);
     } else if (c.kind == MMI_HEAD_2D) {
       for (int a = 0; a < g.n; ++a)
         for (int b2 = 0; b2 < g.n; ++b2) {
           if (a == b2)
-            check_op(c.intra[g.mod[a]], {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH, MMI_OP_GRID},
-                     "a 2D-Boundary intra pair", h);
+            check_op(c.intra[g.mod[a]], {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH, MMI_OP_GRID, MMI_OP_SF_FIXED,
+                                         MMI_OP_SF_STRIDED, MMI_OP_TRISHAPE}, "a 2D-Boundary intra pair", h);
           else
             check_op(c.cross[g.mod[a]][g.mod[b2]], {MMI_OP_NONE, MMI_OP_DENSE, MMI_OP_VERT},
                      "a 2D-Boundary cross pair", h);
@@ -475,6 +481,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
       d.kind = o.kind;
       d.sink = o.sink; d.local = o.local;
       d.use_h = o.use_h != 0; d.use_v = o.use_v != 0; d.use_s = o.use_s != 0;
+      d.stride = o.stride_lo; d.bottom = o.bottom;
       return d;
     };
     if (c.kind == MMI_HEAD_GLOBAL) {

@@ -17,8 +17,11 @@ from typing import Dict, Optional, Tuple
 
 # Operation kinds (same integer codes as include/mmi.h MMI_OP_*).
 OP_NONE, OP_DENSE, OP_ASHAPE, OP_VSLASH, OP_GRID, OP_VERT = 0, 1, 2, 3, 4, 5
+OP_SF_FIXED, OP_SF_STRIDED, OP_TRISHAPE = 6, 7, 8      # static baselines (Section 4.1)
 OP_NAMES = {OP_NONE: "none", OP_DENSE: "dense", OP_ASHAPE: "ashape",
-            OP_VSLASH: "vslash", OP_GRID: "grid", OP_VERT: "vert"}
+            OP_VSLASH: "vslash", OP_GRID: "grid", OP_VERT: "vert",
+            OP_SF_FIXED: "sf_fixed", OP_SF_STRIDED: "sf_strided", OP_TRISHAPE: "trishape"}
+STATIC_OPS = (OP_DENSE, OP_ASHAPE, OP_SF_FIXED, OP_SF_STRIDED, OP_TRISHAPE)
 
 # Head kinds (include/mmi.h MMI_HEAD_*): a global op over all rows (the
 # No-Boundary / K-Boundary case of Section 3.2), Q-Boundary, 2D-Boundary.
@@ -41,6 +44,7 @@ class Op:
     use_h: bool = False
     use_v: bool = False
     use_s: bool = False
+    bottom: int = 0
 
 
 def dense() -> Op:
@@ -57,6 +61,24 @@ def ashape(sink: int, local: int) -> Op:
 
 def vslash(n_vertical: int, n_slash: int) -> Op:
     return Op(OP_VSLASH, n_vertical=n_vertical, n_slash=n_slash)
+
+
+def sf_fixed(segment: int, stride: int) -> Op:
+    """Sparse Transformer "fixed": attend within the own segment of `segment`
+    tokens and to every key at a multiple of `stride` (the segments' first
+    tokens when stride == segment)."""
+    return Op(OP_SF_FIXED, local=segment, stride_lo=stride)
+
+
+def sf_strided(local: int, stride: int) -> Op:
+    """Sparse Transformer "strided": a local window plus every key at a
+    distance that is a multiple of `stride` (dilated slash lines)."""
+    return Op(OP_SF_STRIDED, local=local, stride_lo=stride)
+
+
+def trishape(sink: int, local: int, bottom: int) -> Op:
+    """A-shape plus full attention for the final `bottom` queries."""
+    return Op(OP_TRISHAPE, sink=sink, local=local, bottom=bottom)
 
 
 def vert(n: int) -> Op:

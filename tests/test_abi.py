@@ -32,8 +32,8 @@ def test_every_declared_symbol_is_exported():
 
 def test_struct_sizes_match_header():
     # offsets of the trailing fields fix the layout of everything before them
-    assert ct.sizeof(mmi.mmi_op) == 40
-    assert ct.sizeof(mmi.mmi_head_cfg) == 4 + 40 + 8 * 40 + 64 * 40
+    assert ct.sizeof(mmi.mmi_op) == 44
+    assert ct.sizeof(mmi.mmi_head_cfg) == 4 + 44 + 8 * 44 + 64 * 44
     assert mmi.mmi_problem.modality.offset == 88 and ct.sizeof(mmi.mmi_problem) == 104
 
 

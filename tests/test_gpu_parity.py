@@ -85,6 +85,26 @@ def test_boundary_heads_small(ctx):
     say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
 
 
+def test_static_baselines(ctx):
+    """Section 4.1 baselines as block sets on the same kernel: Sparse
+    Transformer fixed / strided and Tri-shape as global heads (frame-sized
+    parameters) and as Q-Boundary / 2D-Boundary modality ops."""
+    say("[gpu] static baselines")
+    S = 3000
+    mod = _mm_layout(S, 5)
+    q, k, v = _rand_qkv(S, 6, 2, seed=13, scale_k=2.0)
+    heads = [
+        C.global_head(C.sf_fixed(196, 196)),
+        C.global_head(C.sf_strided(196, 196)),
+        C.global_head(C.trishape(128, 512, 128)),
+        C.qboundary_head({0: C.trishape(32, 200, 100), 1: C.sf_strided(64, 150)}),
+        C.boundary2d_head({0: C.sf_fixed(100, 37), 1: C.grid(20, 40)}, {(0, 1): C.vert(40), (1, 0): C.dense()}),
+        C.boundary2d_head({0: C.trishape(0, 64, 300), 1: C.sf_strided(30, 90)}, {(0, 1): C.dense(), (1, 0): C.none()}),
+    ]
+    rep = full_check(ctx, S, 6, 2, mod, heads, q, k, v)
+    say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
+
+
 def test_determinism(ctx):
     say("[gpu] determinism")
     from paper_2504_16083_amd import mmi

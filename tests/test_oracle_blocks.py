@@ -94,8 +94,20 @@ def _random_layout(rng, S, nmod=2, minseg=1, maxseg=300):
     return np.concatenate(segs)
 
 
-def _rand_identity_op(rng, L, allow=("dense", "ashape", "vslash")):
+def _rand_static_op(rng, L):
+    k = int(rng.integers(0, 3))
+    if k == 0:
+        return P.OpState(C.OP_SF_FIXED, C.sf_fixed(int(rng.integers(1, 300)), int(rng.integers(1, 300))), L=L)
+    if k == 1:
+        return P.OpState(C.OP_SF_STRIDED, C.sf_strided(int(rng.integers(1, 300)), int(rng.integers(1, 300))), L=L)
+    return P.OpState(C.OP_TRISHAPE, C.trishape(int(rng.integers(0, 200)), int(rng.integers(0, 300)),
+                                               int(rng.integers(0, 200))), L=L)
+
+
+def _rand_identity_op(rng, L, allow=("dense", "ashape", "vslash", "static")):
     k = allow[int(rng.integers(0, len(allow)))]
+    if k == "static":
+        return _rand_static_op(rng, L)
     if k == "dense":
         return P.OpState(C.OP_DENSE, C.dense(), L=L)
     if k == "ashape":
@@ -206,3 +218,43 @@ def test_permutations_are_bijections():
             back = np.zeros(S)
             back[live] = y[perm >= 0]
             assert np.array_equal(back, x)
+
+
+def test_static_baselines_closed_form_and_reductions():
+    """Sparse Transformer fixed / strided and Tri-shape (Section 4.1 baselines):
+    closed forms == lift over small and frame-sized parameters, and the
+    reductions that make them dense or A-shape."""
+    for L in (300, 1000, 64 * 9 + 5):
+        for seg, stride in [(64, 64), (100, 7), (1, 1), (256, 256), (33, 200), (L + 3, 50)]:
+            _same(_id_plan(L, P.OpState(C.OP_SF_FIXED, C.sf_fixed(seg, stride), L=L)))
+        for local, stride in [(64, 64), (100, 7), (1, 1), (256, 256), (10, 130), (5, L + 1)]:
+            _same(_id_plan(L, P.OpState(C.OP_SF_STRIDED, C.sf_strided(local, stride), L=L)))
+        for sink, local, bottom in [(128, 256, 128), (0, 64, 0), (7, 1, 500), (0, 0, 1), (200, 0, 64)]:
+            _same(_id_plan(L, P.OpState(C.OP_TRISHAPE, C.trishape(sink, local, bottom), L=L)))
+        dense = [np.arange(i + 1) for i in range((L + 63) // 64)]
+        for st in (P.OpState(C.OP_SF_FIXED, C.sf_fixed(L, 1), L=L),          # one segment / every key a head
+                   P.OpState(C.OP_SF_STRIDED, C.sf_strided(1, 1), L=L),       # every distance
+                   P.OpState(C.OP_TRISHAPE, C.trishape(0, 0, L), L=L)):       # every query is final
+            hp = _id_plan(L, st)
+            assert all(np.array_equal(a, b) for a, b in zip(hp.blocks, dense)), st.kind
+        a = _id_plan(L, P.OpState(C.OP_ASHAPE, C.ashape(128, 256), L=L))
+        t = _id_plan(L, P.OpState(C.OP_TRISHAPE, C.trishape(128, 256, 0), L=L))
+        assert all(np.array_equal(x, y) for x, y in zip(a.blocks, t.blocks))
+
+
+def test_static_baselines_known_blocks():
+    """Hand-derived block sets at S = 512 (8 blocks of 64)."""
+    L = 512
+    # fixed, segment = stride = 128: own two-block segment (causal) + block 0 and 2, 4, 6 (heads)
+    hp = _id_plan(L, P.OpState(C.OP_SF_FIXED, C.sf_fixed(128, 128), L=L))
+    assert [b.tolist() for b in hp.blocks] == [[0], [0, 1], [0, 2], [0, 2, 3], [0, 2, 4], [0, 2, 4, 5],
+                                              [0, 2, 4, 6], [0, 2, 4, 6, 7]]
+    # strided, local 64, stride 192: block 7 (q in [448, 511]) sees keys q-63..q (blocks 6, 7),
+    # q-192 (block 4) and q-384 (block 1)
+    hp = _id_plan(L, P.OpState(C.OP_SF_STRIDED, C.sf_strided(64, 192), L=L))
+    assert hp.blocks[7].tolist() == [1, 4, 6, 7]
+    assert hp.blocks[3].tolist() == [0, 2, 3]
+    # Tri-shape sink 64, local 64, bottom 64: the last block sees everything
+    hp = _id_plan(L, P.OpState(C.OP_TRISHAPE, C.trishape(64, 64, 64), L=L))
+    assert hp.blocks[7].tolist() == list(range(8))
+    assert hp.blocks[5].tolist() == [0, 4, 5]
