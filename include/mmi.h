@@ -85,6 +85,11 @@ extern "C" {
 #define MMI_HEAD_GLOBAL 0     /* one op over all rows: No-Boundary / K-Boundary (Sec. 3.2) */
 #define MMI_HEAD_QBOUNDARY 1  /* Algorithm 2: queries grouped by modality, op per modality */
 #define MMI_HEAD_2D 2         /* Algorithm 3: Q and K grouped by modality, op per pair    */
+/* No-Boundary and K-Boundary heads (Section 3.2; Appendix B.1): the sparse
+ * index stays continuous along the query axis, so the head's intra-modality
+ * op applies to all rows at no extra cost. Both names are the global kind. */
+#define MMI_HEAD_NO_BOUNDARY MMI_HEAD_GLOBAL
+#define MMI_HEAD_K_BOUNDARY MMI_HEAD_GLOBAL
 
 typedef struct mmi_op {
   int32_t kind;                  /* MMI_OP_* */
@@ -99,7 +104,13 @@ typedef struct mmi_head_cfg {
   int32_t kind;                  /* MMI_HEAD_* */
   mmi_op global;                 /* HEAD_GLOBAL: DENSE, ASHAPE, VSLASH, GRID or a static baseline */
   mmi_op intra[MMI_MAX_MODALITIES];
-  /* QBOUNDARY: intra[m] in DENSE, ASHAPE, VSLASH or a static baseline (global positions).
+  /* QBOUNDARY: intra[m] in DENSE, ASHAPE, VSLASH, GRID or a static baseline (global
+   * positions; VSLASH and GRID estimated from modality m's final queries). A GRID
+   * modality's queries are ordered by phase and its keys are read in the Grid order
+   * of all S positions: the head's key slots are key layouts of ceil(S/64) blocks
+   * each, position order first (if some modality is not GRID), then one Grid order
+   * per GRID modality in ascending m. layouts * ceil(S/64) must not exceed
+   * MMI_MAX_SEQ / 64 (MMI_ERR_UNSUPPORTED otherwise).
    * 2D: intra[m] in DENSE, ASHAPE, VSLASH, GRID or a static baseline (modality-local
    * coordinates). Static baselines: SF_FIXED, SF_STRIDED (local >= 1, stride_lo >= 1),
    * TRISHAPE (sink, local, bottom >= 0). */
@@ -151,7 +162,7 @@ typedef struct mmi_plan_timing {
 
 /* export kinds for mmi_plan_export (host copies; the call synchronises) */
 #define MMI_EXPORT_QPERM 0       /* int32[n_qblocks*64]: slot -> position or -1 */
-#define MMI_EXPORT_KPERM 1       /* int32[n_kblocks*64] */
+#define MMI_EXPORT_KPERM 1       /* int32[n_kblocks*64] (Q-Boundary with GRID: the layouts in order) */
 #define MMI_EXPORT_ROW_PTR 2     /* int32[n_qblocks+1] */
 #define MMI_EXPORT_COL_IDX 3     /* int32[nnz_blocks], ascending within a row */
 #define MMI_EXPORT_V_SCORES 4    /* float[L_c]: column scores of the estimate */

@@ -22,7 +22,7 @@ horizontal lines become the last query blocks and the vertical lines the
 rightmost key blocks (Algorithm 1: "only the last and rightmost block"):
 the group order is p_g+1, p_g+2, ..., p_g (mod sigma).
 
-Pinned in tests/test_oracle_grid.py: planted periods and phases are
+Pinned in tests/test_oracle_core.py: planted periods and phases are
 recovered, divisors lose, multiples tie toward the smaller stride, the
 permutation is a bijection and sigma = 1 is the identity.
 """

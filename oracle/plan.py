@@ -17,9 +17,15 @@ Head kinds (Sections 3.1-3.2):
     permuted by phase), or one of the static baselines of Section 4.1
     (Sparse Transformer fixed / strided, Tri-shape; identity order);
   * Q-Boundary (Algorithm 2): queries grouped by modality (each group padded
-    to a multiple of B), keys in original order; each modality's queries use
-    their own op in global positions, estimated from that modality's final
-    queries;
+    to a multiple of B); each modality's queries use their own op in global
+    positions, estimated from that modality's final queries. A Grid modality
+    (stride and phase searched on global positions) orders its queries by
+    phase (group order p+1, ..., p, position order inside a phase) and reads
+    the keys in the Grid order of all S positions (Algorithm 5's strided key
+    loads). Keys therefore come in key layouts: the position order (if some
+    modality is not Grid) followed by one Grid order per Grid modality in
+    ascending modality id, each padded to a multiple of B and concatenated;
+    a query block only selects key blocks of its modality's layout;
   * 2D-Boundary (Algorithm 3): queries and keys grouped by modality; inside a
     group tokens are in Grid order when that modality's op is Grid, else in
     position order; each (query modality, key modality) pair has its own op:
@@ -90,6 +96,7 @@ class HeadPlan:
     ops: dict = field(default_factory=dict)          # key -> OpState
     folds: dict = field(default_factory=dict)        # key -> {sigma: fp32 fold}
     groups: dict = field(default_factory=dict)       # m -> (slot offset, T_m in group order)
+    kbase: dict = field(default_factory=dict)        # Q-Boundary: m -> first key block of its layout
     mod: object = None
 
     @property
@@ -160,13 +167,14 @@ def choose(cfg: C.HeadCfg, S: int, modality, q_rows, K: np.ndarray, scale=None):
     if cfg.kind == C.HEAD_QBOUNDARY:
         for m in mods:
             op = cfg.intra_op(m)
-            if op.kind not in C.STATIC_OPS + (C.OP_VSLASH,):
-                raise NotImplementedError("Q-Boundary intra op must be VS or a static pattern")
+            if op.kind not in C.STATIC_OPS + (C.OP_VSLASH, C.OP_GRID):
+                raise NotImplementedError("Q-Boundary intra op must be VS, Grid or a static pattern")
             e = None
-            if op.kind == C.OP_VSLASH:
+            if op.kind in (C.OP_GRID, C.OP_VSLASH):
                 rows = layout.final_run_rows(T[m])
                 e = est[("q", m)] = _estimate(q_rows, K, rows, scale, None, rows)
-            ops[("q", m)] = _resolve(op, S, e, None)
+            folds[("q", m)] = {}
+            ops[("q", m)] = _resolve(op, S, e, folds[("q", m)])
         return ops, est, folds
     if cfg.kind == C.HEAD_2D:
         for m in mods:
@@ -217,13 +225,27 @@ def assemble(kind: int, S: int, modality, ops: dict) -> HeadPlan:
         arr = T[m]
         if kind == C.HEAD_2D and ops[("i", m)].kind == C.OP_GRID:
             arr = T[m][ops[("i", m)].cos]
+        if kind == C.HEAD_QBOUNDARY and ops[("q", m)].kind == C.OP_GRID:
+            st = ops[("q", m)]
+            rank = (arr - st.p - 1) % st.sigma          # phase p+1 first, phase p last
+            arr = arr[np.lexsort((arr, rank))]
         hp.groups[m] = (off, arr)
         part = pad_to_block(arr.copy())
         parts.append(part)
         off += len(part)
     hp.qperm = np.concatenate(parts)
     if kind == C.HEAD_QBOUNDARY:
-        hp.kperm = pad_to_block(np.arange(S, dtype=np.int64))
+        grid_mods = [m for m in sorted(T) if ops[("q", m)].op.kind == C.OP_GRID]
+        layouts = ([None] if len(grid_mods) < len(T) else []) + grid_mods
+        nb = (S + B - 1) // B
+        segs = []
+        for m in layouts:
+            st = None if m is None else ops[("q", m)]
+            order = st.cos if st is not None and st.kind == C.OP_GRID else np.arange(S, dtype=np.int64)
+            segs.append(pad_to_block(order.copy()))
+        hp.kperm = np.concatenate(segs)
+        for m in T:
+            hp.kbase[m] = layouts.index(m if m in grid_mods else None) * nb
         hp.blocks = [_qb_row(hp, i) for i in range(hp.nbq)]
     elif kind == C.HEAD_2D:
         hp.kperm = hp.qperm.copy()
@@ -345,15 +367,38 @@ def _group_of_block(hp: HeadPlan, i: int):
     raise IndexError(i)
 
 
+def _qb_grid_blocks(st: OpState, rows: np.ndarray, kbase: int):
+    """Grid closed forms for query positions `rows` (any set of positions)
+    against keys in the Grid order of all S positions: coordinate c sits at
+    slot g0[c mod sigma] + c // sigma."""
+    s, p, g0 = st.sigma, st.p, st.g0
+    ph = rows % s
+    out = set(blk(g0[ph] + rows // s).tolist())          # forced: each row's own key
+    if st.op.use_s:                                      # same phase, k <= q
+        for f in np.unique(ph).tolist():
+            qmax = int(rows[ph == f].max())
+            out.update(range(blk(int(g0[f])), blk(int(g0[f]) + qmax // s) + 1))
+    maxq = int(rows.max())
+    if st.op.use_v and maxq >= p:                        # phase-p keys, k <= q
+        out.update(range(blk(int(g0[p])), blk(int(g0[p]) + (maxq - p) // s) + 1))
+    if st.op.use_h and (ph == p).any():                  # phase-p rows see every k <= q
+        qh = int(rows[ph == p].max())
+        out.update(np.nonzero(_block_min(st) <= qh)[0].tolist())
+    return {kbase + j for j in out}
+
+
 def _qb_row(hp: HeadPlan, i: int):
     m, off, Tm = _group_of_block(hp, i)
     lo = i * B - off
     rows = Tm[lo:lo + B]
-    runs = _runs(rows)
     st = hp.ops[("q", m)]
-    bs = _identity_op_blocks(st, runs, 0)
+    kbase = hp.kbase[m]
+    if st.kind == C.OP_GRID:
+        return np.array(sorted(_qb_grid_blocks(st, rows, kbase)), dtype=np.int64)
+    runs = _runs(rows)
+    bs = _identity_op_blocks(st, runs, kbase)
     for a, b in runs:                       # forced: each row's own key block
-        bs.update(range(blk(a), blk(b) + 1))
+        bs.update(range(kbase + blk(a), kbase + blk(b) + 1))
     return np.array(sorted(bs), dtype=np.int64)
 
 
@@ -458,16 +503,30 @@ def token_predicate(hp: HeadPlan, qpos: np.ndarray, kpos: np.ndarray) -> np.ndar
     return out
 
 
+def _key_span(hp: HeadPlan, i: int):
+    """Key slots [lo, hi) that query block i reads: its modality's key layout
+    for a Q-Boundary head, all key slots otherwise."""
+    if hp.kind == C.HEAD_QBOUNDARY:
+        m = _group_of_block(hp, i)[0]
+        nb = (hp.S + B - 1) // B
+        return hp.kbase[m] * B, (hp.kbase[m] + nb) * B
+    return 0, len(hp.kperm)
+
+
 def lift_blocks(hp: HeadPlan):
     """BS by enumeration: causal pairs satisfying the predicate, plus each
     row's own key block."""
-    kslot_of = np.full(hp.S, -1, dtype=np.int64)
-    valid_k = hp.kperm >= 0
-    kslot_of[hp.kperm[valid_k]] = np.nonzero(valid_k)[0]
-    kvalid = np.nonzero(valid_k)[0]
-    kpos = hp.kperm[kvalid]
+    spans = {}
     out = []
     for i in range(hp.nbq):
+        span = _key_span(hp, i)
+        if span not in spans:
+            seg = hp.kperm[span[0]:span[1]]
+            live = np.nonzero(seg >= 0)[0]
+            kslot_of = np.full(hp.S, -1, dtype=np.int64)
+            kslot_of[seg[live]] = span[0] + live
+            spans[span] = (span[0] + live, seg[live], kslot_of)
+        kvalid, kpos, kslot_of = spans[span]
         rows = hp.qperm[i * B:(i + 1) * B]
         rows = rows[rows >= 0]
         m = token_predicate(hp, rows, kpos) & (kpos[None, :] <= rows[:, None])

@@ -26,6 +26,7 @@ STATIC_OPS = (OP_DENSE, OP_ASHAPE, OP_SF_FIXED, OP_SF_STRIDED, OP_TRISHAPE)
 # Head kinds (include/mmi.h MMI_HEAD_*): a global op over all rows (the
 # No-Boundary / K-Boundary case of Section 3.2), Q-Boundary, 2D-Boundary.
 HEAD_GLOBAL, HEAD_QBOUNDARY, HEAD_2D = 0, 1, 2
+HEAD_NO_BOUNDARY = HEAD_K_BOUNDARY = HEAD_GLOBAL   # index continuous along queries (Appendix B.1)
 
 MAX_STRIDE = 1024          # Table "search space": max stride
 MAX_MODALITIES = 8
@@ -115,6 +116,17 @@ class HeadCfg:
 
 def global_head(op: Op) -> HeadCfg:
     return HeadCfg(HEAD_GLOBAL, op=op)
+
+
+def no_boundary_head(op: Op) -> HeadCfg:
+    """No modality boundary: the intra-modality op over all rows."""
+    return HeadCfg(HEAD_NO_BOUNDARY, op=op)
+
+
+def k_boundary_head(op: Op) -> HeadCfg:
+    """Boundaries along the key axis only: the index is continuous along the
+    query axis, so the intra-modality op applies over all rows (Appendix B.1)."""
+    return HeadCfg(HEAD_K_BOUNDARY, op=op)
 
 
 def qboundary_head(intra: Dict[int, Op]) -> HeadCfg:

@@ -258,3 +258,88 @@ def test_static_baselines_known_blocks():
     hp = _id_plan(L, P.OpState(C.OP_TRISHAPE, C.trishape(64, 64, 64), L=L))
     assert hp.blocks[7].tolist() == list(range(8))
     assert hp.blocks[5].tolist() == [0, 4, 5]
+
+
+def _rand_qb_grid_ops(rng, S, mod):
+    """Per modality: a Grid state on global positions (some resolved to the
+    dense fallback) or a random identity-order op."""
+    ops = {}
+    for m in np.unique(mod).tolist():
+        r = rng.random()
+        if r < 0.45:
+            s = int(rng.integers(1, min(70, S // 2) + 1))
+            f = FLAGS[int(rng.integers(0, 8))]
+            ops[("q", m)] = P.grid_state(C.grid(s, s, *f), S, s, int(rng.integers(0, s)))
+        elif r < 0.55:
+            ops[("q", m)] = P.OpState(C.OP_DENSE, C.grid(4, 8), L=S)       # Grid search found no stride
+        else:
+            ops[("q", m)] = _rand_identity_op(rng, S)
+    return ops
+
+
+def test_qboundary_grid_closed_form_random_layouts():
+    """Q-Boundary heads with Grid modalities: closed forms == literal lift,
+    key layouts (position order first when some modality is not Grid, then
+    one Grid order per Grid modality) and per-block layout confinement."""
+    rng = np.random.default_rng(11)
+    for trial in range(30):
+        S = int(rng.integers(150, 1400))
+        mod = _random_layout(rng, S, nmod=int(rng.integers(2, 4)), maxseg=int(rng.integers(5, 400)))
+        ops = _rand_qb_grid_ops(rng, S, mod)
+        hp = P.assemble(C.HEAD_QBOUNDARY, S, mod, ops)
+        _same(hp)
+        nb = (S + 63) // 64
+        mods = sorted(ops)
+        grid_mods = [m for (_, m) in mods if ops[("q", m)].op.kind == C.OP_GRID]
+        nlay = len(grid_mods) + (len(grid_mods) < len(mods))
+        assert len(hp.kperm) == nlay * nb * 64
+        for ell in range(nlay):
+            seg = hp.kperm[ell * nb * 64:(ell + 1) * nb * 64]
+            assert sorted(seg[seg >= 0].tolist()) == list(range(S))
+        for i, bs in enumerate(hp.blocks):
+            m = P._group_of_block(hp, i)[0]
+            assert ((bs >= hp.kbase[m]) & (bs < hp.kbase[m] + nb)).all()
+
+
+def test_qboundary_grid_query_order_and_global_reduction():
+    """A Grid modality's queries follow the Grid order of all positions
+    restricted to that modality; with one modality the head is the global
+    Grid head (same permutations, same blocks)."""
+    rng = np.random.default_rng(12)
+    for trial in range(10):
+        S = int(rng.integers(200, 1200))
+        mod = _random_layout(rng, S, nmod=3, maxseg=250)
+        s = int(rng.integers(2, 50))
+        st = P.grid_state(C.grid(s, s), S, s, int(rng.integers(0, s)))
+        mg = int(mod[-1])
+        ops = {("q", m): (st if m == mg else P.OpState(C.OP_DENSE, C.dense(), L=S)) for m in np.unique(mod).tolist()}
+        hp = P.assemble(C.HEAD_QBOUNDARY, S, mod, ops)
+        assert np.array_equal(hp.groups[mg][1], st.cos[mod[st.cos] == mg])
+    for s, p in ((1, 0), (7, 3), (64, 63), (100, 17)):
+        for f in FLAGS:
+            st = P.grid_state(C.grid(s, s, *f), 900, s, p)
+            g = P.assemble(C.HEAD_GLOBAL, 900, None, {"g": st})
+            q = P.assemble(C.HEAD_QBOUNDARY, 900, None, {("q", 0): st})
+            assert np.array_equal(q.qperm, g.qperm) and np.array_equal(q.kperm, g.kperm)
+            assert all(np.array_equal(a, b) for a, b in zip(q.blocks, g.blocks))
+
+
+def test_qboundary_grid_known_blocks():
+    """Hand-derived: S = 256, modality 0 on [0, 64), modality 1 on [64, 256)
+    with Grid sigma = 2, phase 1, vertical lines only. Keys in Grid order:
+    phase 0 (even positions) in slots 0..127, phase 1 (odd) in 128..255.
+    Modality-1 queries: even positions 64..254 (slots 0..95 of its group),
+    then odd 65..255. Query block 0 (even 64..190): own keys at slots 32..95
+    -> key blocks 0, 1; vertical (odd keys <= 190, slots 128..222) -> 2, 3.
+    Block 1 (even 192..254, odd 65..127): own keys at slots 96..127 and
+    160..191 -> key blocks 1, 2; vertical (odd keys <= 254) -> 2, 3."""
+    S = 256
+    mod = np.array([0] * 64 + [1] * 192, dtype=np.uint8)
+    st = P.grid_state(C.grid(2, 2, h=False, v=True, s=False), S, 2, 1)
+    ops = {("q", 0): P.OpState(C.OP_ASHAPE, C.ashape(0, 64), L=S), ("q", 1): st}
+    hp = P.assemble(C.HEAD_QBOUNDARY, S, mod, ops)
+    assert hp.kbase == {0: 0, 1: 4}
+    assert hp.blocks[0].tolist() == [0]
+    assert hp.blocks[1].tolist() == [4 + 0, 4 + 1, 4 + 2, 4 + 3]
+    assert hp.blocks[2].tolist() == [4 + 1, 4 + 2, 4 + 3]
+    _same(hp)

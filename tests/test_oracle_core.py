@@ -174,3 +174,30 @@ def test_topk_matches_sort_brute_force():
     # only the visible prefix competes
     x = np.arange(10, dtype=np.float32)
     assert vslash.topk(x, 3, 6).tolist() == [3, 4, 5]
+
+
+def test_qboundary_grid_choice_from_the_modality_final_queries():
+    """Q-Boundary Grid: the stride and phase come from the final queries of
+    that modality against global key positions. Planted: keys at positions
+    = 7 (mod 24) share a direction that only the video queries (positions
+    [256, 1536)) carry; text queries carry another, with lines every 10
+    positions. Video finds (24, 7) over global positions; the text modality
+    (last run [1536, 1600)) finds (10, 3)."""
+    from oracle import plan as P
+    from synth import config as C
+    S, D = 1600, 16
+    rng = np.random.default_rng(9)
+    mod = np.array([0] * 256 + [1] * 1280 + [0] * 64, dtype=np.uint8)
+    K = 0.01 * rng.standard_normal((S, D))
+    Q = 0.01 * rng.standard_normal((S, D))
+    K[7::24, 0] += 3.0
+    K[3::10, 1] += 3.0
+    Q[mod == 1, 0] = 3.0
+    Q[mod == 0, 1] = 3.0
+    cfg = C.qboundary_head({0: C.grid(8, 40), 1: C.grid(16, 40)})
+    ops, est, folds = P.choose(cfg, S, mod, lambda r: Q[r], K, scale=1.0)
+    assert np.array_equal(est[("q", 1)].rows, np.arange(1472, 1536))
+    assert np.array_equal(est[("q", 0)].rows, np.arange(1536, 1600))
+    assert (ops[("q", 1)].sigma, ops[("q", 1)].p) == (24, 7)
+    assert (ops[("q", 0)].sigma, ops[("q", 0)].p) == (10, 3)
+    assert est[("q", 1)].L_c == 1536 and len(ops[("q", 1)].cos) == S
