@@ -121,6 +121,13 @@ struct Groups {
   int32_t toff[MMI_MAX_MODALITIES];   // offset of T_m inside the position pool
 };
 
+struct QbOrderJob {   // phase order of one Q-Boundary Grid modality's queries
+  const int32_t* params;      // the op's {sigma, phase} (sigma <= 1: position order stays)
+  int32_t* qperm;             // the head's qperm at the modality group's slot offset
+  int32_t mod;                // modality id
+  int32_t* cnt;               // [qb_order_chunks(S)] scratch: counts, then offsets
+};
+
 struct WorkItem {
   int32_t head, group, e0, e1;   // union entries [e0, e1) of row group `group`
   int32_t part;       // -1: write O directly; else partial slot
@@ -133,10 +140,15 @@ struct SplitRow {     // a row group whose union list is split over several item
 
 // ---------------------------------------------------------------- launches
 // k_layout.hip
+// modpos (nullable): [S] modality id of every position
 hipError_t launch_positions(const Segment* segs, int nseg, const int32_t* toff_by_mod, int32_t* tpos,
-                            int S, hipStream_t st);
+                            uint8_t* modpos, int S, hipStream_t st);
+// max_slots >= every head's nbq*64 and nbk*64
 hipError_t launch_perms(const HeadDev* heads, int nheads, const OpDev* ops, Groups g,
-                        const int32_t* tpos, int S, int max_nbq_slots, hipStream_t st);
+                        const int32_t* tpos, int S, int max_slots, hipStream_t st);
+// after launch_perms: Q-Boundary Grid modalities' queries in phase order
+hipError_t launch_qb_order(const QbOrderJob* jobs, int njobs, const uint8_t* modpos, int S, hipStream_t st);
+int qb_order_chunks(int S);
 // k_estimate.hip
 hipError_t launch_est_lse(const RowSet* rs, int nrs, int max_chunks, Tensor q, Tensor k,
                           int chunk_keys, hipStream_t st);

@@ -90,6 +90,16 @@ __device__ __forceinline__ void set_range(uint32_t* bm, int a, int b) {
   }
 }
 
+// one thread sets the bits [a, b]
+__device__ __forceinline__ void set_range_one(uint32_t* bm, int a, int b) {
+  for (int w = a >> 5; w <= (b >> 5); ++w) {
+    uint32_t m = 0xffffffffu;
+    if (w == (a >> 5)) m &= 0xffffffffu << (a & 31);
+    if (w == (b >> 5)) m &= 0xffffffffu >> (31 - (b & 31));
+    atomicOr(&bm[w], m);
+  }
+}
+
 // key blocks [kbase, kbase + n) whose threshold value thr[j - kbase] <= lim
 __device__ __forceinline__ void set_threshold(uint32_t* bm, const int32_t* thr, int kbase, int n, int lim,
                                               bool identity_blocks) {
@@ -168,6 +178,34 @@ __device__ void grid_rules(uint32_t* bm, const OpDev& op, int sig, int ph, int L
   __syncthreads();
 }
 
+// Q-Boundary Grid: query rows rpos[0, nvalid) of one modality in phase
+// order (global positions), keys in the Grid order of all S positions at key
+// block kbase + slot / 64 (coordinate c sits at slot g0(c mod s) + c / s).
+__device__ void qb_grid_rules(uint32_t* bm, const OpDev& op, int sig, int ph, int S, const int* rpos, int nvalid,
+                              int maxpos, const int32_t* kminpos, int kbase, int* sh_qh) {
+  const GridGeo geo = grid_geo(S, sig, ph);
+  if (threadIdx.x == 0) *sh_qh = -1;
+  __syncthreads();
+  const int r = threadIdx.x;
+  if (r < nvalid) {
+    const int q = rpos[r], f = q % sig;
+    const int g0f = grid_g0(geo, f);
+    set_bit(bm, kbase + (g0f + q / sig) / B);                        // the row's own key
+    // rows of one phase are contiguous and ascending: the last one reaches furthest
+    if (op.use_s && (r + 1 == nvalid || rpos[r + 1] % sig != f))     // same phase, k <= q
+      set_range_one(bm, kbase + g0f / B, kbase + (g0f + q / sig) / B);
+    if (f == ph) atomicMax(sh_qh, q);
+  }
+  if (op.use_v && maxpos >= ph) {                                    // phase-p keys, k <= q
+    const int g0p = grid_g0(geo, ph);
+    set_range(bm, kbase + g0p / B, kbase + (g0p + (maxpos - ph) / sig) / B);
+  }
+  __syncthreads();
+  const int qh = *sh_qh;
+  if (op.use_h && qh >= 0) set_threshold(bm, kminpos + kbase, kbase, (S + B - 1) / B, qh, false);
+  __syncthreads();
+}
+
 __global__ __launch_bounds__(256) void k_blocks_count(const HeadDev* heads, const OpDev* ops, Groups g) {
   const HeadDev hd = heads[blockIdx.x];
   const int qb = blockIdx.y;
@@ -225,8 +263,13 @@ __global__ __launch_bounds__(256) void k_blocks_count(const HeadDev* heads, cons
     if (tid == 0) set_bit(bm, qb);
   } else if (hd.kind == MMI_HEAD_QBOUNDARY) {
     const OpDev op = ops[hd.op0 + gi];
-    identity_rules(bm, op, ra, rb, nruns, maxpos, 0);
-    for (int r = 0; r < nruns; ++r) set_range(bm, ra[r] / B, rb[r] / B);
+    const int sig = op.kind == MMI_OP_GRID ? op.params[0] : 0;
+    if (sig > 0) {
+      qb_grid_rules(bm, op, sig, op.params[1], hd.S, rpos, sh_nvalid, maxpos, hd.kminpos, op.kbase, &sh_maxc);
+    } else {
+      identity_rules(bm, op, ra, rb, nruns, maxpos, op.kbase);
+      for (int r = 0; r < nruns; ++r) set_range(bm, op.kbase + ra[r] / B, op.kbase + rb[r] / B);
+    }
   } else {
     for (int gk = 0; gk < g.n; ++gk) {
       const OpDev op = ops[hd.op0 + gi * g.n + gk];

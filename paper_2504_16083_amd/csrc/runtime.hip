@@ -392,6 +392,19 @@ struct Builder {
   }
 };
 
+// Key layouts of a Q-Boundary head: the position order (if some modality is
+// not Grid) and one Grid order per Grid modality.
+static int qb_grid_mods(const Groups& g, const mmi_head_cfg& c) {
+  int n = 0;
+  for (int gi = 0; gi < g.n; ++gi) n += c.intra[g.mod[gi]].kind == MMI_OP_GRID;
+  return n;
+}
+
+static int qb_layouts(const Groups& g, const mmi_head_cfg& c) {
+  const int n = qb_grid_mods(g, c);
+  return n + (n < g.n ? 1 : 0);
+}
+
 static void validate_cfgs(const Groups& g, const mmi_problem& p, const mmi_head_cfg* cfgs) {
   for (int h = 0; h < p.Hq; ++h) {
     const mmi_head_cfg& c = cfgs[h];
@@ -400,8 +413,13 @@ static void validate_cfgs(const Groups& g, const mmi_problem& p, const mmi_head_
                           MMI_OP_SF_STRIDED, MMI_OP_TRISHAPE}, "a global head", h);
     } else if (c.kind == MMI_HEAD_QBOUNDARY) {
       for (int gi = 0; gi < g.n; ++gi)
-        check_op(c.intra[g.mod[gi]], {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH, MMI_OP_SF_FIXED, MMI_OP_SF_STRIDED,
-                                      MMI_OP_TRISHAPE}, "a Q-Boundary modality", h);
+        check_op(c.intra[g.mod[gi]], {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH, MMI_OP_GRID, MMI_OP_SF_FIXED,
+                                      MMI_OP_SF_STRIDED, MMI_OP_TRISHAPE}, "a Q-Boundary modality", h);
+      const int nlay = qb_layouts(g, c);
+      const int64_t nb = (p.S + B - 1) / B;
+      if (nlay > 1 && nlay * nb > MMI_MAX_SEQ / B)
+        fail(MMI_ERR_UNSUPPORTED, "head %d: %d key layouts of %lld blocks exceed %d key blocks", h, nlay,
+             (long long)nb, MMI_MAX_SEQ / B);
     } else if (c.kind == MMI_HEAD_2D) {
       for (int a = 0; a < g.n; ++a)
         for (int b2 = 0; b2 < g.n; ++b2) {
@@ -456,7 +474,11 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   Segment* d_segs = upload(P, L.segs);
   int32_t* d_toff = upload(P, toff_by_mod);
   bd.d_tpos = P->d_tpos = dalloc<int32_t>(P, S);
-  HIPCHK(launch_positions(d_segs, (int)L.segs.size(), d_toff, bd.d_tpos, S, st));
+  bool qb_grid = false;
+  for (int h = 0; h < p.Hq; ++h) qb_grid |= cfgs[h].kind == MMI_HEAD_QBOUNDARY && qb_grid_mods(g, cfgs[h]) > 0;
+  uint8_t* d_modpos = qb_grid ? dalloc<uint8_t>(P, S) : nullptr;
+  HIPCHK(launch_positions(d_segs, (int)L.segs.size(), d_toff, bd.d_tpos, d_modpos, S, st));
+  std::vector<QbOrderJob> qjobs;
 
   const int nb_all = (S + B - 1) / B;
   int nb_groups = 0;
@@ -516,14 +538,30 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
       H.op_slot.push_back(0);
     } else if (c.kind == MMI_HEAD_QBOUNDARY) {
       hd.nbq = nb_groups;
-      hd.nbk = nb_all;
       hd.qperm = dalloc<int32_t>(P, (size_t)nb_groups * B);
+      const int ngrid = qb_grid_mods(g, c);
+      hd.nbk = ngrid ? qb_layouts(g, c) * nb_all : nb_all;
+      if (ngrid) {          // key layouts: [position order] then one Grid order per Grid modality
+        hd.kperm = dalloc<int32_t>(P, (size_t)hd.nbk * B);
+        hd.kminpos = dalloc<int32_t>(P, hd.nbk);
+        hd.kmaxpos = dalloc<int32_t>(P, hd.nbk);
+      }
+      int next_layout = ngrid < g.n ? 1 : 0;
       for (int gi = 0; gi < g.n; ++gi) {
         const mmi_op& o = c.intra[g.mod[gi]];
         OpDev d = base_op(o);
-        d.L = S; d.kbase = 0; d.nkblk = nb_all;
+        d.L = S; d.nkblk = nb_all;
+        d.kbase = o.kind == MMI_OP_GRID ? (next_layout++) * nb_all : 0;
         EstInfo e;
-        if (o.kind == MMI_OP_VSLASH) {
+        if (o.kind == MMI_OP_GRID) {
+          int row0, nrows, loc0;
+          final_rows(L, gi, row0, nrows, loc0);
+          e = bd.est(h, hd.kvh, row0, nrows, row0, -1, row0 + nrows, false);
+          int32_t* params = dalloc<int32_t>(P, 4);
+          bd.grid(e, o, params);
+          d.params = params;
+          qjobs.push_back({params, hd.qperm + g.off[gi], g.mod[gi], dalloc<int32_t>(P, qb_order_chunks(S))});
+        } else if (o.kind == MMI_OP_VSLASH) {
           int row0, nrows, loc0;
           final_rows(L, gi, row0, nrows, loc0);
           e = bd.est(h, hd.kvh, row0, nrows, row0, -1, row0 + nrows, true);
@@ -620,7 +658,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
     hd.itembase = dalloc<int32_t>(P, hd.gcap);
     hd.splitoff = dalloc<int32_t>(P, hd.gcap);
     hd.partoff = dalloc<int32_t>(P, hd.gcap);
-    max_slots = std::max(max_slots, hd.nbq * B);
+    max_slots = std::max(max_slots, std::max(hd.nbq, hd.nbk) * B);
     max_nbq = std::max(max_nbq, hd.nbq);
     max_groups = std::max(max_groups, hd.gcap);
     max_nbk = std::max(max_nbk, hd.nbk);
@@ -647,6 +685,8 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   P->d_heads = upload(P, P->heads);
   P->d_ops = upload(P, P->ops);
   HIPCHK(launch_perms(P->d_heads, p.Hq, P->d_ops, g, bd.d_tpos, S, max_slots, st));
+  QbOrderJob* d_qj = upload(P, qjobs);
+  HIPCHK(launch_qb_order(d_qj, (int)qjobs.size(), d_modpos, S, st));
   HIPCHK(launch_key_summaries(P->d_heads, p.Hq, P->d_ops, (int)P->ops.size(), g, max_nbk, bd.max_sel, st));
   const int chunk = ctx->chunk_blocks;
   HIPCHK(launch_blocks_count(P->d_heads, p.Hq, P->d_ops, g, max_nbq, st));

@@ -58,7 +58,14 @@ def test_validation_codes_without_device():
     assert _create(mmi.Problem(100, 2, 1), [C.global_head(C.grid(5, 2000))] * 2) == -3
     assert _create(mmi.Problem(100, 2, 1), [C.global_head(C.vert(5))] * 2) == -3
     mod = np.zeros(100, np.uint8); mod[50:] = 1
-    assert _create(mmi.Problem(100, 2, 1, mod), [C.qboundary_head({1: C.grid(4, 8)})] * 2) == -3
+    assert _create(mmi.Problem(100, 2, 1, mod), [C.qboundary_head({1: C.grid(0, 8)})] * 2) == -3
+    assert _create(mmi.Problem(100, 2, 1, mod), [C.qboundary_head({1: C.grid(4, 8)})] * 2) == -1  # valid
+    big = np.zeros(1 << 21, np.uint8); big[1 << 20:] = 1      # 2 key layouts x 32768 blocks
+    assert _create(mmi.Problem(1 << 21, 2, 1, big), [C.qboundary_head({1: C.grid(4, 8)})] * 2) == -2
+    assert "key layouts" in mmi.mmi_last_error()
+    assert _create(mmi.Problem(1 << 21, 2, 1, big), [C.qboundary_head({0: C.grid(4, 8), 1: C.grid(4, 8)})] * 2) == -2
+    assert _create(mmi.Problem(1 << 20, 2, 1, big[1 << 19:3 << 19].copy()),       # 2 x 16384 blocks: fits
+                   [C.qboundary_head({1: C.grid(4, 8)})] * 2) == -1
     bad2d = C.boundary2d_head({0: C.dense(), 1: C.dense()}, {(0, 1): C.ashape(1, 1)})
     assert _create(mmi.Problem(100, 2, 1, mod), [bad2d] * 2) == -3
     assert "cross" in mmi.mmi_last_error()

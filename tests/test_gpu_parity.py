@@ -105,6 +105,39 @@ def test_static_baselines(ctx):
     say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
 
 
+def test_qboundary_grid(ctx):
+    """Grid as a Q-Boundary modality op: stride and phase from the modality's
+    final queries on global positions, phase-ordered queries, keys through
+    one Grid layout per Grid modality (with and without the position-order
+    layout), on a text/video layout with 196-token frames."""
+    from synth.generate import Structure, Workload
+    say("[gpu] Q-Boundary Grid")
+    S, F = 16384, 196
+    rng = np.random.default_rng(17)
+    segs, n, m = [], 0, 0
+    while n < S:
+        ln = int(rng.integers(300, 900)) if m == 0 else F * int(rng.integers(8, 30))
+        ln = min(ln, S - n)
+        segs.append(np.full(ln, m, np.uint8))
+        n += ln
+        m ^= 1
+    mod = np.concatenate(segs)
+    st = Structure(sigma=[F, F], amp=2.0, text_amp=1.0)
+    st.line_slot = [int(rng.integers(0, F)) for _ in range(2)]
+    heads = [
+        C.qboundary_head({0: C.ashape(128, 1024), 1: C.grid_frame(F)}),
+        C.qboundary_head({0: C.vslash(100, 64), 1: C.grid_window(F)}),
+        C.qboundary_head({0: C.grid(8, 64), 1: C.grid_frame(F)}),
+        C.qboundary_head({0: C.dense(), 1: C.grid(F - 4, F + 4, True, False, False)}),
+    ]
+    wl = Workload("qb_grid_16k", S, 4, 2, mod, heads, st, 20250416 + 17, frame=F)
+    q, k, v = generate.make_qkv(wl, "cuda")
+    rows = np.unique(np.concatenate([np.arange(S - 64, S), np.random.default_rng(2).choice(S, 512, replace=False)]))
+    rep = full_check(ctx, S, 4, 2, mod, heads, q, k, v, rows=rows)
+    say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g}")
+    assert len(rep.ties) <= 1
+
+
 def test_determinism(ctx):
     say("[gpu] determinism")
     from paper_2504_16083_amd import mmi
