@@ -65,9 +65,10 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8)
     ap.add_argument("--pattern", default="method",
-                    choices=["method", "ashape", "trishape", "sf_fixed", "sf_strided", "vslash"],
-                    help="every head on one of the paper's baseline patterns (Section 4.1, baseline "
-                         "hyperparameter table) instead of the workload's per-head patterns")
+                    choices=["method", "ashape", "trishape", "sf_fixed", "sf_strided", "vslash", "qb_grid"],
+                    help="every head on one pattern instead of the workload's per-head patterns: one of "
+                         "the paper's baselines (Section 4.1, baseline hyperparameter table), or qb_grid "
+                         "(Q-Boundary heads, A-shape text and Grid video)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain copy of this many MiB (k_permute, identity) before the steps, "
                          "as the reference dispatch for HBM byte counters")
@@ -135,10 +136,13 @@ def main():
     if args.pattern != "method":
         from synth import config as C
         tpf = wl.frame or 256        # tokens per frame
-        op = {"ashape": C.ashape(128, 4096), "trishape": C.trishape(128, 4096, 128),
-              "sf_fixed": C.sf_fixed(tpf, tpf), "sf_strided": C.sf_strided(tpf, tpf),
-              "vslash": C.vslash(1000, 1024)}[args.pattern]
-        wl.heads = [C.global_head(op)] * wl.Hq
+        head = {"ashape": C.global_head(C.ashape(128, 4096)),
+                "trishape": C.global_head(C.trishape(128, 4096, 128)),
+                "sf_fixed": C.global_head(C.sf_fixed(tpf, tpf)),
+                "sf_strided": C.global_head(C.sf_strided(tpf, tpf)),
+                "vslash": C.global_head(C.vslash(1000, 1024)),
+                "qb_grid": C.qboundary_head({0: C.ashape(128, 4096), 1: C.grid_window(tpf)})}[args.pattern]
+        wl.heads = [head] * wl.Hq
         wl.name = f"{wl.name}+{args.pattern}"
     torch.cuda.set_device(0)
     log(f"workload {wl.name}: S={wl.S} Hq={wl.Hq} Hkv={wl.Hkv}")

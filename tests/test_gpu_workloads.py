@@ -138,3 +138,17 @@ def test_row_group_unions(ctx):
             np.testing.assert_array_equal(uent, ent)
     finally:
         plan.destroy()
+
+
+def test_qboundary_grid_1m(ctx):
+    """Q-Boundary heads with A-shape text and Grid video on the 1M layout:
+    two key layouts of 16384 blocks each, the most the block index holds.
+    Block index bit-exact, O/LSE on sampled rows, two heads of different KV
+    groups."""
+    wl = workloads.by_id(4)
+    wl.heads = [C.qboundary_head({0: C.ashape(128, 4096), 1: C.grid_window(wl.frame)}) for _ in range(wl.Hq)]
+    say(f"[gpu] Q-Boundary Grid on {wl.name}")
+    q, k, v = generate.make_qkv(wl, "cuda")
+    rep = sampled_check(ctx, wl, q, k, v, [0, 27])
+    say(f"  rows={rep.rows} ties={rep.ties} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g} nnz={rep.nnz}")
+    assert len(rep.ties) <= 1
