@@ -1,7 +1,8 @@
 """Masked softmax attention in fp64 (the computation of Algorithms 5-7).
 
 For a query at position q with the element mask M(q) of its head plan
-(selected blocks, causal by original positions):
+(selected blocks, causal by original positions unless the head is
+bidirectional):
     O[q]   = sum_{k in M(q)} softmax_k(tau * q.k) V[k]
     LSE[q] = ln sum_{k in M(q)} exp(tau * q.k)
 Skipped keys contribute exactly zero. This is the plain definition; the
@@ -42,7 +43,7 @@ def head_rows(hp: P.HeadPlan, Qh, K, V, rows, scale=None):
     for n, q in enumerate(rows):
         i = int(slot_of[q]) // P.B
         ks = np.concatenate([hp.kperm[j * P.B:(j + 1) * P.B] for j in hp.blocks[i]])
-        keys = np.sort(ks[(ks >= 0) & (ks <= q)])
+        keys = np.sort(ks[(ks >= 0) & ((ks <= q) | (not hp.causal))])
         O[n], L[n] = attend(qv[n], K, V, keys, scale)
     return O, L
 
@@ -80,7 +81,9 @@ def permuted_blockwise(hp: P.HeadPlan, Qh, K, V, scale=None):
             kc = K[np.maximum(kpos, 0)]
             vc = V[np.maximum(kpos, 0)]
             s = scale * (qc @ kc.T)
-            ok = (kpos[None, :] >= 0) & (kpos[None, :] <= qpos[:, None]) & live[:, None]
+            ok = (kpos[None, :] >= 0) & live[:, None]
+            if hp.causal:
+                ok &= kpos[None, :] <= qpos[:, None]
             s = np.where(ok, s, -np.inf)
             m_new = np.maximum(m, s.max(axis=1))
             safe = np.where(np.isfinite(m_new), m_new, 0.0)

@@ -15,7 +15,9 @@ Head kinds (Sections 3.1-3.2):
   * global op (No-Boundary / K-Boundary heads, applied to all rows):
     dense, A-shape, Vertical-Slash (identity order) or Grid (Algorithm 1:
     permuted by phase), or one of the static baselines of Section 4.1
-    (Sparse Transformer fixed / strided, Tri-shape; identity order);
+    (Sparse Transformer fixed / strided, Tri-shape; identity order), or
+    neighborhood attention over a token grid (Appendix F; tile order,
+    bidirectional: the only head without the causal condition);
   * Q-Boundary (Algorithm 2): queries grouped by modality (each group padded
     to a multiple of B); each modality's queries use their own op in global
     positions, estimated from that modality's final queries. A Grid modality
@@ -46,7 +48,7 @@ import numpy as np
 
 from synth import config as C
 
-from . import estimate, grid, layout, vslash
+from . import estimate, grid, layout, natten, vslash
 
 B = 64
 
@@ -98,6 +100,7 @@ class HeadPlan:
     groups: dict = field(default_factory=dict)       # m -> (slot offset, T_m in group order)
     kbase: dict = field(default_factory=dict)        # Q-Boundary: m -> first key block of its layout
     mod: object = None
+    causal: bool = True                              # False only for neighborhood attention
 
     @property
     def nbq(self):
@@ -211,6 +214,16 @@ def assemble(kind: int, S: int, modality, ops: dict) -> HeadPlan:
     hp = HeadPlan(kind, S, None, None, mod=mod, ops=ops)
     if kind == C.HEAD_GLOBAL:
         st = ops["g"]
+        if st.kind == C.OP_NATTEN:
+            o = st.op
+            assert int(np.prod(o.grid)) == S and int(np.prod(o.tile)) == B
+            hp.causal = False
+            hp.qperm = natten.permutation(o.grid, o.tile)
+            hp.kperm = hp.qperm.copy()
+            hp.groups[0] = (0, hp.qperm[hp.qperm >= 0])
+            hp.blocks = [np.array(natten.tile_blocks(o.grid, o.win, o.tile, i), dtype=np.int64)
+                         for i in range(hp.nbq)]
+            return hp
         if st.kind == C.OP_GRID:
             perm = pad_to_block(st.cos.copy())
         else:
@@ -476,6 +489,8 @@ def _op_pred(st: OpState, qc, kc):
     if st.kind == C.OP_GRID:
         o = st.op
         return grid.predicate(qc, kc, st.sigma, st.p, o.use_h, o.use_v, o.use_s)
+    if st.kind == C.OP_NATTEN:
+        return natten.predicate(qc, kc, st.op.grid, st.op.win)
     raise ValueError(st.kind)
 
 
@@ -529,7 +544,9 @@ def lift_blocks(hp: HeadPlan):
         kvalid, kpos, kslot_of = spans[span]
         rows = hp.qperm[i * B:(i + 1) * B]
         rows = rows[rows >= 0]
-        m = token_predicate(hp, rows, kpos) & (kpos[None, :] <= rows[:, None])
+        m = token_predicate(hp, rows, kpos)
+        if hp.causal:
+            m &= kpos[None, :] <= rows[:, None]
         hit = kvalid[m.any(axis=0)]
         bs = set(blk(hit).tolist()) | set(blk(kslot_of[rows]).tolist())
         out.append(np.array(sorted(bs), dtype=np.int64))
@@ -537,10 +554,12 @@ def lift_blocks(hp: HeadPlan):
 
 
 def element_mask_row(hp: HeadPlan, q: int) -> np.ndarray:
-    """Positions k (ascending) that query position q attends to (D1/D2)."""
+    """Positions k (ascending) that query position q attends to: every key of
+    its selected blocks, causal (k <= q) unless the head is bidirectional."""
     x = int(np.nonzero(hp.qperm == q)[0][0])
     keys = []
+    lim = q if hp.causal else hp.S
     for j in hp.blocks[x // B]:
         ks = hp.kperm[j * B:(j + 1) * B]
-        keys.append(ks[(ks >= 0) & (ks <= q)])
+        keys.append(ks[(ks >= 0) & (ks <= lim)])
     return np.sort(np.concatenate(keys)) if keys else np.zeros(0, np.int64)

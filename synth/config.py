@@ -18,9 +18,11 @@ from typing import Dict, Optional, Tuple
 # Operation kinds (same integer codes as include/mmi.h MMI_OP_*).
 OP_NONE, OP_DENSE, OP_ASHAPE, OP_VSLASH, OP_GRID, OP_VERT = 0, 1, 2, 3, 4, 5
 OP_SF_FIXED, OP_SF_STRIDED, OP_TRISHAPE = 6, 7, 8      # static baselines (Section 4.1)
+OP_NATTEN = 9              # 2D/3D neighborhood attention through a tile permutation (Appendix F)
 OP_NAMES = {OP_NONE: "none", OP_DENSE: "dense", OP_ASHAPE: "ashape",
             OP_VSLASH: "vslash", OP_GRID: "grid", OP_VERT: "vert",
-            OP_SF_FIXED: "sf_fixed", OP_SF_STRIDED: "sf_strided", OP_TRISHAPE: "trishape"}
+            OP_SF_FIXED: "sf_fixed", OP_SF_STRIDED: "sf_strided", OP_TRISHAPE: "trishape",
+            OP_NATTEN: "natten"}
 STATIC_OPS = (OP_DENSE, OP_ASHAPE, OP_SF_FIXED, OP_SF_STRIDED, OP_TRISHAPE)
 
 # Head kinds (include/mmi.h MMI_HEAD_*): a global op over all rows (the
@@ -46,6 +48,9 @@ class Op:
     use_v: bool = False
     use_s: bool = False
     bottom: int = 0
+    grid: tuple = (0, 0, 0)        # NATTEN token grid (T, H, W), raster order, W fastest
+    win: tuple = (0, 0, 0)         # NATTEN neighborhood size per axis (odd)
+    tile: tuple = (0, 0, 0)        # NATTEN permutation tile, product 64
 
 
 def dense() -> Op:
@@ -80,6 +85,47 @@ def sf_strided(local: int, stride: int) -> Op:
 def trishape(sink: int, local: int, bottom: int) -> Op:
     """A-shape plus full attention for the final `bottom` queries."""
     return Op(OP_TRISHAPE, sink=sink, local=local, bottom=bottom)
+
+
+def natten(grid, win, tile=None) -> Op:
+    """Neighborhood attention over a (T, H, W) token grid (T = 1 for images),
+    bidirectional: each token sees the win_t x win_h x win_w neighborhood
+    around it, shifted inside the grid at the borders. Tokens are permuted
+    tile by tile (tile_t x tile_h x tile_w = 64 tokens = one block); the
+    default tile is the one with the fewest selected blocks."""
+    grid, win = tuple(int(x) for x in grid), tuple(int(x) for x in win)
+    if tile is None:
+        tile = natten_best_tile(grid, win)
+    return Op(OP_NATTEN, grid=grid, win=win, tile=tuple(int(x) for x in tile))
+
+
+def natten_tiles():
+    """Tile shapes (powers of two, 64 tokens)."""
+    return [(1 << a, 1 << b, 1 << (6 - a - b)) for a in range(7) for b in range(7 - a)]
+
+
+def natten_best_tile(grid, win):
+    """Tile with the fewest selected (query tile, key tile) pairs: per axis the
+    key-tile span of every query tile, multiplied over the axes (smallest
+    padding on ties). Host-side choice of an input parameter; the block sets
+    themselves come from the library and the oracle."""
+    best = None
+    for tile in natten_tiles():
+        pairs, slots = 1, 1
+        for n, k, t in zip(grid, win, tile):
+            nt = -(-n // t)
+            span = 0
+            for a in range(nt):
+                c0, c1 = a * t, min(n, a * t + t) - 1
+                lo = min(max(c0 - k // 2, 0), n - k)
+                hi = min(max(c1 - k // 2, 0), n - k) + k - 1
+                span += hi // t - lo // t + 1
+            pairs *= span
+            slots *= nt * t
+        key = (pairs, slots)
+        if best is None or key < best[0]:
+            best = (key, tile)
+    return best[1]
 
 
 def vert(n: int) -> Op:
