@@ -60,6 +60,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=4, help="workload id 0-4 (4 = 1M tokens)")
+    ap.add_argument("--workload", default="mm", choices=["mm", "natten"],
+                    help="mm: the multi-modal prefill workloads (--config); natten: neighborhood "
+                         "attention over a video DiT token grid (Appendix F), bidirectional")
     ap.add_argument("--dense-reps", type=int, default=1)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
@@ -132,7 +135,7 @@ def main():
     from synth import config as C
     from synth import generate, workloads
 
-    wl = workloads.by_id(args.config)
+    wl = workloads.natten_video() if args.workload == "natten" else workloads.by_id(args.config)
     if args.pattern != "method":
         from synth import config as C
         tpf = wl.frame or 256        # tokens per frame
@@ -192,12 +195,23 @@ def main():
     attn_tflops = blocks * FLOP_PER_BLOCK / (avg["attn_ms"] * 1e-3) / 1e12
     nb = (wl.S + 63) // 64
     causal_blocks = nb * (nb + 1) // 2 * wl.Hq
+    dense_heads = [C.global_head(C.dense())] * wl.Hq
+    if args.workload == "natten":
+        # bidirectional baseline: the same op with windows as large as the grid
+        # allows (odd), which selects every (query tile, key tile) pair
+        g, t = wl.extra["grid"], wl.extra["tile"]
+        full = C.natten(g, tuple(n if n % 2 else n - 1 for n in g), t)
+        dense_heads = [C.global_head(full)] * wl.Hq
+        ntiles = 1
+        for n, x in zip(g, t):
+            ntiles *= -(-n // x)
+        causal_blocks = ntiles * ntiles * wl.Hq
 
     dense = None
     if not args.no_dense:
         dense_ms, dense_attn = [], []
         for _ in range(args.dense_reps):
-            plan = mmi.Plan(ctx, prob, [C.global_head(C.dense())] * wl.Hq, q, k, stream)
+            plan = mmi.Plan(ctx, prob, dense_heads, q, k, stream)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             plan.execute(q, k, v, o, lse, stream)
@@ -225,14 +239,20 @@ def main():
         cpu = cpu_baseline(wl, q, k, v, args.cpu_rows, heads)
 
     out = {
-        "metric": "prefill attention ms/layer (sparse, all heads, estimation + index + attention)",
+        "metric": ("neighborhood attention ms/layer (bidirectional, all heads, index + attention)"
+                   if args.workload == "natten" else
+                   "prefill attention ms/layer (sparse, all heads, estimation + index + attention)"),
         "value": ms, "unit": "ms/layer", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms, "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic (seeded Q/K/V with planted grid/text/sink structure)",
+        "dtype": "bf16",
+        "data": ("synthetic (seeded N(0,1) Q/K/V)" if args.workload == "natten"
+                 else "synthetic (seeded Q/K/V with planted grid/text/sink structure)"),
         "config": {"workload": wl.name, "S": wl.S, "Hq": wl.Hq, "Hkv": wl.Hkv, "head_dim": 128,
-                   "block": 64, "parallelism": "single GPU"},
+                   "block": 64, "parallelism": "single GPU",
+                   **({k2: wl.extra[k2] for k2 in ("grid", "win", "tile")} if args.workload == "natten" else {})},
         "stages_ms": {k2: avg[k2] for k2 in ("est_ms", "select_ms", "index_ms", "attn_ms", "combine_ms")},
-        "blocks": {"computed": blocks, "loaded": loaded, "causal": causal_blocks,
+        "blocks": {"computed": blocks, "loaded": loaded,
+                   ("all_pairs" if args.workload == "natten" else "causal"): causal_blocks,
                    "density": blocks / causal_blocks, "computed_per_load": blocks / max(loaded, 1)},
         "roofline": {"bound": "mfma", "kernel": "k_attention", "achieved": attn_tflops,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": attn_tflops / PEAK_BF16_TFLOPS,

@@ -80,6 +80,16 @@ extern "C" {
 #define MMI_OP_TRISHAPE 8    /* A-shape plus every key for the final `bottom` queries:     */
                              /* k < sink or q - k < local or q >= L - bottom (L = extent   */
                              /* of the op's coordinates: S, or the modality's length)      */
+/* Neighborhood attention over a token grid (Appendix F: the 2D/3D sliding windows
+ * of DiT models made block-dense by a permutation). Global heads only; the one
+ * bidirectional op (no k <= q condition). Tokens form a grid_t x grid_h x grid_w
+ * grid in raster order (position (t*grid_h + h)*grid_w + w; grid_t = 1 for
+ * images). Along an axis of length n with odd window k, coordinate c sees the k
+ * coordinates from min(max(c - k/2, 0), n - k). Queries and keys are permuted
+ * tile by tile (tile_t x tile_h x tile_w = 64 tokens, tiles and the tokens inside
+ * a tile in raster order, border tiles padded), so tile i is block i; query tile
+ * i selects every key tile that meets the union of its tokens' windows. */
+#define MMI_OP_NATTEN 9
 
 /* Head kinds. */
 #define MMI_HEAD_GLOBAL 0     /* one op over all rows: No-Boundary / K-Boundary (Sec. 3.2) */
@@ -98,11 +108,15 @@ typedef struct mmi_op {
   int32_t stride_lo, stride_hi;  /* GRID: 1 <= lo <= hi <= MMI_MAX_STRIDE */
   int32_t use_h, use_v, use_s;   /* GRID line flags (0/1) */
   int32_t bottom;                /* TRISHAPE: final queries with full attention, >= 0 */
+  int32_t grid_t, grid_h, grid_w;  /* NATTEN: token grid, product == S */
+  int32_t win_t, win_h, win_w;     /* NATTEN: odd window per axis, 1 <= win <= grid */
+  int32_t tile_t, tile_h, tile_w;  /* NATTEN: permutation tile, each >= 1, product 64; the
+                                      number of tiles must not exceed MMI_MAX_SEQ / 64 */
 } mmi_op;
 
 typedef struct mmi_head_cfg {
   int32_t kind;                  /* MMI_HEAD_* */
-  mmi_op global;                 /* HEAD_GLOBAL: DENSE, ASHAPE, VSLASH, GRID or a static baseline */
+  mmi_op global;                 /* HEAD_GLOBAL: DENSE, ASHAPE, VSLASH, GRID, NATTEN or a static baseline */
   mmi_op intra[MMI_MAX_MODALITIES];
   /* QBOUNDARY: intra[m] in DENSE, ASHAPE, VSLASH, GRID or a static baseline (global
    * positions; VSLASH and GRID estimated from modality m's final queries). A GRID

@@ -80,10 +80,12 @@ struct OpDev {
   int32_t kgrid;              // key group is Grid-ordered (VERT into a Grid group)
   const int32_t* kparams;     // that group's {sigma, phase}
   int32_t koff;               // key group slot offset
+  int32_t grid[3], win[3], tile[3];   // NATTEN token grid, window, permutation tile
 };
 
 struct HeadDev {
   int32_t kind, kvh;
+  int32_t causal;             // 0: bidirectional (NATTEN), only padding keys are masked
   int32_t nbq, nbk;           // permuted query / key blocks
   int32_t S;
   int32_t* qperm;             // [nbq*64] or nullptr (identity)

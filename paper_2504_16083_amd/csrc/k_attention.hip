@@ -273,6 +273,12 @@ struct WaveState {
   int qpos, rb, c, h, vlane;
 };
 
+// Mask threshold of a wave's rows: keys above it are masked. A bidirectional
+// head masks only padding keys (position INT_BIG).
+__device__ __forceinline__ int mask_limit(const WaveState& ws, bool causal) {
+  return causal || ws.qpos < 0 ? ws.qpos : INT_BIG - 1;
+}
+
 __device__ __forceinline__ bool sel(int e, int rb) { return (e >> (16 + rb)) & 1; }
 __device__ __forceinline__ bool needs_mask(int e, int rb) { return (e >> (24 + rb)) & 1; }
 
@@ -369,7 +375,7 @@ __device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, cons
 // s_sm, `regs` loading block t+3, kpn the key positions of block t+4. The
 // step multiplies P(t)V(t), turns the scores of t+1 into P(t+1) (p_new),
 // computes the scores of t+2 into s_qk, stages t+3 and starts loading t+4.
-template <int R, bool PERM>
+template <int R, bool PERM, bool CAUSAL>
 __device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const KeySrc<R>& ks,
                                            BlockRegs<R>& regs, int (&kpn)[Tile<R>::L], int tid, int t, int n,
                                            int e0, int e1, int e2, int e5, f32x16 (&s_qk)[2],
@@ -382,7 +388,7 @@ __device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const KeyS
   const Stage& kst = stg[(t + 2) & (NSTAGE - 1)];
   float alpha = 1.0f;
   if (a1) {
-    if (needs_mask(e1, ws.rb)) mask_block(stg[(t + 1) & (NSTAGE - 1)], ws.qpos, ws.h, s_sm);
+    if (needs_mask(e1, ws.rb)) mask_block(stg[(t + 1) & (NSTAGE - 1)], mask_limit(ws, CAUSAL), ws.h, s_sm);
     if (a2 && a0) fused_step<true, true>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
     else if (a2) fused_step<true, false>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
     else if (a0) fused_step<false, true>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
@@ -405,7 +411,7 @@ __device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const KeyS
   __syncthreads();
 }
 
-template <int R, bool PERM>
+template <int R, bool PERM, bool CAUSAL>
 __device__ __forceinline__ void block_loop(WaveState& ws, Stage* stg, const AttnArgs& a, const HeadDev& hd,
                                            const WorkItem& w, int tid) {
   KeySrc<R> ks;
@@ -439,7 +445,7 @@ __device__ __forceinline__ void block_loop(WaveState& ws, Stage* stg, const Attn
   bf16x8 pa[4], pb[4];
   if (sel(e0, ws.rb)) {
     qk_block(stg[0], ws.qr, ws.c, ws.h, sa);
-    if (needs_mask(e0, ws.rb)) mask_block(stg[0], ws.qpos, ws.h, sa);
+    if (needs_mask(e0, ws.rb)) mask_block(stg[0], mask_limit(ws, CAUSAL), ws.h, sa);
     float alpha;
     softmax_block(sa, sc, ws.m, ws.l, pa, alpha);
   }
@@ -447,11 +453,11 @@ __device__ __forceinline__ void block_loop(WaveState& ws, Stage* stg, const Attn
   // two steps per trip so that the buffers swap roles without copies
   for (int t = 0; t < n; t += 2) {
     int e5 = es.get(t + 5);
-    block_step<R, PERM>(ws, stg, ks, regs, kpn, tid, t, n, e0, e1, e2, e5, sa, pa, sb, pb, sc);
+    block_step<R, PERM, CAUSAL>(ws, stg, ks, regs, kpn, tid, t, n, e0, e1, e2, e5, sa, pa, sb, pb, sc);
     e0 = e1; e1 = e2; e2 = e3; e3 = e4; e4 = e5;
     if (t + 1 >= n) break;
     e5 = es.get(t + 6);
-    block_step<R, PERM>(ws, stg, ks, regs, kpn, tid, t + 1, n, e0, e1, e2, e5, sb, pb, sa, pa, sc);
+    block_step<R, PERM, CAUSAL>(ws, stg, ks, regs, kpn, tid, t + 1, n, e0, e1, e2, e5, sb, pb, sa, pa, sc);
     e0 = e1; e1 = e2; e2 = e3; e3 = e4; e4 = e5;
   }
 }
@@ -490,8 +496,9 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
     for (int e = 0; e < 16; ++e) ws.o[dt][e] = 0.0f;
   ws.m = NEG_BIG;
   ws.l = 0.0f;
-  if (hd.kperm) block_loop<R, true>(ws, stg, a, hd, w, tid);
-  else block_loop<R, false>(ws, stg, a, hd, w, tid);
+  if (!hd.causal) block_loop<R, true, false>(ws, stg, a, hd, w, tid);
+  else if (hd.kperm) block_loop<R, true, true>(ws, stg, a, hd, w, tid);
+  else block_loop<R, false, true>(ws, stg, a, hd, w, tid);
 
   const float m = ws.m, l = ws.l;
   const int qpos = ws.qpos, h = ws.h;

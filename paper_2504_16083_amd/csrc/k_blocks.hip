@@ -178,6 +178,26 @@ __device__ void grid_rules(uint32_t* bm, const OpDev& op, int sig, int ph, int L
   __syncthreads();
 }
 
+// Neighborhood attention, query tile qb (tiles in raster order, one block
+// each): per axis the union of the windows of the tile's coordinates is one
+// interval; every key tile meeting the product of the intervals is selected.
+__device__ void natten_rules(uint32_t* bm, const OpDev& op, int qb) {
+  int nt[3], lo[3], hi[3];
+  for (int a = 0; a < 3; ++a) nt[a] = (op.grid[a] + op.tile[a] - 1) / op.tile[a];
+  const int idx[3] = {qb / (nt[1] * nt[2]), (qb / nt[2]) % nt[1], qb % nt[2]};
+  for (int a = 0; a < 3; ++a) {
+    const int n = op.grid[a], k = op.win[a], t = op.tile[a];
+    const int c0 = idx[a] * t, c1 = min(n, c0 + t) - 1;
+    lo[a] = min(max(c0 - k / 2, 0), n - k) / t;
+    hi[a] = (min(max(c1 - k / 2, 0), n - k) + k - 1) / t;
+  }
+  const int rows = (hi[0] - lo[0] + 1) * (hi[1] - lo[1] + 1);
+  for (int r = threadIdx.x; r < rows; r += blockDim.x) {      // one run of key tiles per (t, h) tile row
+    const int x = lo[0] + r / (hi[1] - lo[1] + 1), y = lo[1] + r % (hi[1] - lo[1] + 1);
+    set_range_one(bm, (x * nt[1] + y) * nt[2] + lo[2], (x * nt[1] + y) * nt[2] + hi[2]);
+  }
+}
+
 // Q-Boundary Grid: query rows rpos[0, nvalid) of one modality in phase
 // order (global positions), keys in the Grid order of all S positions at key
 // block kbase + slot / 64 (coordinate c sits at slot g0(c mod s) + c / s).
@@ -256,7 +276,9 @@ __global__ __launch_bounds__(256) void k_blocks_count(const HeadDev* heads, cons
   if (hd.kind == MMI_HEAD_GLOBAL) {
     const OpDev op = ops[hd.op0];
     const int sig = op.kind == MMI_OP_GRID ? op.params[0] : 0;
-    if (sig > 0)
+    if (op.kind == MMI_OP_NATTEN)
+      natten_rules(bm, op, qb);
+    else if (sig > 0)
       grid_rules(bm, op, sig, op.params[1], hd.S, qb, 0, rpos, hd.kminpos, false, &sh_maxc);
     else
       identity_rules(bm, op, ra, rb, nruns, maxpos, 0);
@@ -496,7 +518,8 @@ __global__ __launch_bounds__(256) void k_blocks_fill(const HeadDev* heads) {
 // Union entries of a row group, ascending in the key block: key block in
 // bits 0-15, bit 16+r set if query block r of the group selects it, bit 24+r
 // set if it does and the key block holds a position above the smallest
-// query position of query block r (or padding), i.e. needs the causal mask.
+// query position of query block r (or padding), i.e. needs the causal mask
+// (for a bidirectional head: only if the key block holds padding).
 __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R) {
   const HeadDev hd = heads[blockIdx.x];
   const int gr = blockIdx.y;
@@ -513,7 +536,7 @@ __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R)
     const int r = x / B, slot = rows[r] * B + x % B;
     if (rows[r] >= hd.nbq) continue;
     const int p = hd.qperm ? hd.qperm[slot] : (slot < hd.S ? slot : -1);
-    if (p >= 0) atomicMin(&qmin[r], p);
+    if (p >= 0) atomicMin(&qmin[r], hd.causal ? p : INT_BIG - 1);   // bidirectional: only padding masks
   }
   const int per = (hd.nwords + 255) / 256;
   const int w0 = threadIdx.x * per;

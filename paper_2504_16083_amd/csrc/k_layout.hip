@@ -64,6 +64,18 @@ __device__ int qb_key_pos(const HeadDev& hd, const OpDev* ops, const Groups& g, 
   return xi;
 }
 
+// Position held by slot x of the neighborhood-attention tile order (-1 for
+// the padding of tiles cut by the grid border).
+__device__ int natten_pos(const OpDev& op, int x) {
+  const int nt1 = (op.grid[1] + op.tile[1] - 1) / op.tile[1], nt2 = (op.grid[2] + op.tile[2] - 1) / op.tile[2];
+  const int tile = x / B, in = x % B;
+  const int t = tile / (nt1 * nt2) * op.tile[0] + in / (op.tile[1] * op.tile[2]);
+  const int h = tile / nt2 % nt1 * op.tile[1] + in / op.tile[2] % op.tile[1];
+  const int w = tile % nt2 * op.tile[2] + in % op.tile[2];
+  if (t >= op.grid[0] || h >= op.grid[1] || w >= op.grid[2]) return -1;
+  return (t * op.grid[1] + h) * op.grid[2] + w;
+}
+
 __global__ __launch_bounds__(256) void k_perms(const HeadDev* heads, const OpDev* ops, Groups g,
                                                const int32_t* tpos) {
   const HeadDev hd = heads[blockIdx.x];
@@ -71,7 +83,9 @@ __global__ __launch_bounds__(256) void k_perms(const HeadDev* heads, const OpDev
   if (hd.kind == MMI_HEAD_QBOUNDARY && hd.kperm && x < hd.nbk * B) hd.kperm[x] = qb_key_pos(hd, ops, g, x);
   if (!hd.qperm || x >= hd.nbq * B) return;
   int pos = -1;
-  if (hd.kind == MMI_HEAD_GLOBAL) {
+  if (hd.kind == MMI_HEAD_GLOBAL && ops[hd.op0].kind == MMI_OP_NATTEN) {
+    pos = natten_pos(ops[hd.op0], x);
+  } else if (hd.kind == MMI_HEAD_GLOBAL) {
     const OpDev op = ops[hd.op0];
     const int sig = op.params ? op.params[0] : 0;
     if (x < hd.S) pos = sig > 0 ? grid_coord(grid_geo(hd.S, sig, op.params[1]), x) : x;

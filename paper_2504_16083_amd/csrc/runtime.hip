@@ -392,6 +392,28 @@ struct Builder {
   }
 };
 
+static_assert(sizeof(mmi_op) == 80 && sizeof(mmi_head_cfg) == 4 + 73 * 80, "mmi.h struct layout");
+
+static int natten_tiles(const mmi_op& o) {
+  return ((o.grid_t + o.tile_t - 1) / o.tile_t) * ((o.grid_h + o.tile_h - 1) / o.tile_h) *
+         ((o.grid_w + o.tile_w - 1) / o.tile_w);
+}
+
+static void check_natten(const mmi_op& o, int64_t S, int h) {
+  const int g[3] = {o.grid_t, o.grid_h, o.grid_w}, w[3] = {o.win_t, o.win_h, o.win_w};
+  const int t[3] = {o.tile_t, o.tile_h, o.tile_w};
+  for (int a = 0; a < 3; ++a) {
+    if (g[a] < 1 || t[a] < 1) fail(MMI_ERR_BAD_CONFIG, "head %d: NATTEN grid and tile sizes must be >= 1", h);
+    if (w[a] < 1 || w[a] > g[a] || w[a] % 2 == 0)
+      fail(MMI_ERR_BAD_CONFIG, "head %d: NATTEN window %d on an axis of %d (odd, 1..axis)", h, w[a], g[a]);
+  }
+  if ((int64_t)g[0] * g[1] * g[2] != S)
+    fail(MMI_ERR_BAD_CONFIG, "head %d: NATTEN grid %dx%dx%d != S", h, g[0], g[1], g[2]);
+  if (t[0] * t[1] * t[2] != B) fail(MMI_ERR_BAD_CONFIG, "head %d: NATTEN tile must hold 64 tokens", h);
+  if ((int64_t)natten_tiles(o) > MMI_MAX_SEQ / B)
+    fail(MMI_ERR_UNSUPPORTED, "head %d: %d NATTEN tiles exceed %d blocks", h, natten_tiles(o), MMI_MAX_SEQ / B);
+}
+
 // Key layouts of a Q-Boundary head: the position order (if some modality is
 // not Grid) and one Grid order per Grid modality.
 static int qb_grid_mods(const Groups& g, const mmi_head_cfg& c) {
@@ -410,7 +432,8 @@ static void validate_cfgs(const Groups& g, const mmi_problem& p, const mmi_head_
     const mmi_head_cfg& c = cfgs[h];
     if (c.kind == MMI_HEAD_GLOBAL) {
       check_op(c.global, {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH, MMI_OP_GRID, MMI_OP_SF_FIXED,
-                          MMI_OP_SF_STRIDED, MMI_OP_TRISHAPE}, "a global head", h);
+                          MMI_OP_SF_STRIDED, MMI_OP_TRISHAPE, MMI_OP_NATTEN}, "a global head", h);
+      if (c.global.kind == MMI_OP_NATTEN) check_natten(c.global, p.S, h);
     } else if (c.kind == MMI_HEAD_QBOUNDARY) {
       for (int gi = 0; gi < g.n; ++gi)
         check_op(c.intra[g.mod[gi]], {MMI_OP_DENSE, MMI_OP_ASHAPE, MMI_OP_VSLASH, MMI_OP_GRID, MMI_OP_SF_FIXED,
@@ -504,9 +527,26 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
       d.sink = o.sink; d.local = o.local;
       d.use_h = o.use_h != 0; d.use_v = o.use_v != 0; d.use_s = o.use_s != 0;
       d.stride = o.stride_lo; d.bottom = o.bottom;
+      d.grid[0] = o.grid_t; d.grid[1] = o.grid_h; d.grid[2] = o.grid_w;
+      d.win[0] = o.win_t; d.win[1] = o.win_h; d.win[2] = o.win_w;
+      d.tile[0] = o.tile_t; d.tile[1] = o.tile_h; d.tile[2] = o.tile_w;
       return d;
     };
-    if (c.kind == MMI_HEAD_GLOBAL) {
+    hd.causal = 1;
+    if (c.kind == MMI_HEAD_GLOBAL && c.global.kind == MMI_OP_NATTEN) {
+      // tile-permuted queries and keys, one block per tile, bidirectional
+      hd.nbq = hd.nbk = natten_tiles(c.global);
+      hd.causal = 0;
+      hd.qperm = dalloc<int32_t>(P, (size_t)hd.nbq * B);
+      hd.kperm = hd.qperm;
+      hd.kminpos = dalloc<int32_t>(P, hd.nbk);
+      hd.kmaxpos = dalloc<int32_t>(P, hd.nbk);
+      OpDev d = base_op(c.global);
+      d.L = S; d.kbase = 0; d.nkblk = hd.nbk;
+      P->ops.push_back(d);
+      H.est.push_back(EstInfo{});
+      H.op_slot.push_back(0);
+    } else if (c.kind == MMI_HEAD_GLOBAL) {
       hd.nbq = hd.nbk = nb_all;
       OpDev d = base_op(c.global);
       d.L = S; d.kbase = 0; d.nkblk = nb_all;

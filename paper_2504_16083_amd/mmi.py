@@ -35,7 +35,10 @@ class mmi_op(ct.Structure):
     _fields_ = [("kind", ct.c_int32), ("sink", ct.c_int32), ("local", ct.c_int32),
                 ("n_vertical", ct.c_int32), ("n_slash", ct.c_int32),
                 ("stride_lo", ct.c_int32), ("stride_hi", ct.c_int32),
-                ("use_h", ct.c_int32), ("use_v", ct.c_int32), ("use_s", ct.c_int32), ("bottom", ct.c_int32)]
+                ("use_h", ct.c_int32), ("use_v", ct.c_int32), ("use_s", ct.c_int32), ("bottom", ct.c_int32),
+                ("grid_t", ct.c_int32), ("grid_h", ct.c_int32), ("grid_w", ct.c_int32),
+                ("win_t", ct.c_int32), ("win_h", ct.c_int32), ("win_w", ct.c_int32),
+                ("tile_t", ct.c_int32), ("tile_h", ct.c_int32), ("tile_w", ct.c_int32)]
 
 
 class mmi_head_cfg(ct.Structure):
@@ -136,7 +139,7 @@ def mmi_last_error() -> str:
 # ------------------------------------------------------------------ marshalling
 def op_struct(op: C.Op) -> mmi_op:
     return mmi_op(op.kind, op.sink, op.local, op.n_vertical, op.n_slash, op.stride_lo, op.stride_hi,
-                  int(op.use_h), int(op.use_v), int(op.use_s), op.bottom)
+                  int(op.use_h), int(op.use_v), int(op.use_s), op.bottom, *op.grid, *op.win, *op.tile)
 
 
 def head_cfgs(heads) -> ct.Array:

@@ -32,8 +32,8 @@ def test_every_declared_symbol_is_exported():
 
 def test_struct_sizes_match_header():
     # offsets of the trailing fields fix the layout of everything before them
-    assert ct.sizeof(mmi.mmi_op) == 44
-    assert ct.sizeof(mmi.mmi_head_cfg) == 4 + 44 + 8 * 44 + 64 * 44
+    assert ct.sizeof(mmi.mmi_op) == 80
+    assert ct.sizeof(mmi.mmi_head_cfg) == 4 + 80 + 8 * 80 + 64 * 80
     assert mmi.mmi_problem.modality.offset == 88 and ct.sizeof(mmi.mmi_problem) == 104
 
 
@@ -66,6 +66,14 @@ def test_validation_codes_without_device():
     assert _create(mmi.Problem(1 << 21, 2, 1, big), [C.qboundary_head({0: C.grid(4, 8), 1: C.grid(4, 8)})] * 2) == -2
     assert _create(mmi.Problem(1 << 20, 2, 1, big[1 << 19:3 << 19].copy()),       # 2 x 16384 blocks: fits
                    [C.qboundary_head({1: C.grid(4, 8)})] * 2) == -1
+    nat = lambda grid, win, tile: [C.global_head(C.natten(grid, win, tile))] * 2
+    assert _create(mmi.Problem(100, 2, 1), nat((1, 10, 10), (1, 3, 5), (1, 8, 8))) == -1       # valid
+    assert _create(mmi.Problem(100, 2, 1), nat((1, 10, 10), (1, 4, 5), (1, 8, 8))) == -3       # even window
+    assert _create(mmi.Problem(100, 2, 1), nat((1, 10, 10), (1, 3, 11), (1, 8, 8))) == -3      # window > axis
+    assert _create(mmi.Problem(100, 2, 1), nat((1, 10, 11), (1, 3, 5), (1, 8, 8))) == -3       # grid != S
+    assert _create(mmi.Problem(100, 2, 1), nat((1, 10, 10), (1, 3, 5), (1, 8, 4))) == -3       # tile != 64
+    assert _create(mmi.Problem(100, 2, 1, mod), [C.qboundary_head({0: C.natten((1, 10, 10), (1, 3, 3), (1, 8, 8))})] * 2) == -3
+    assert _create(mmi.Problem(1 << 20, 2, 1), nat((1, 1 << 10, 1 << 10), (1, 3, 3), (64, 1, 1))) == -2  # 2^20 tiles
     bad2d = C.boundary2d_head({0: C.dense(), 1: C.dense()}, {(0, 1): C.ashape(1, 1)})
     assert _create(mmi.Problem(100, 2, 1, mod), [bad2d] * 2) == -3
     assert "cross" in mmi.mmi_last_error()

@@ -138,6 +138,24 @@ def test_qboundary_grid(ctx):
     assert len(rep.ties) <= 1
 
 
+def test_natten(ctx):
+    """Neighborhood attention (bidirectional) through the tile permutation:
+    3D and 2D grids of 2880 tokens, tiles cut by the grid border (padding
+    masked), a near-full window and a 1x1x1 window."""
+    say("[gpu] neighborhood attention")
+    S = 2880
+    q, k, v = _rand_qkv(S, 5, 1, seed=19)
+    heads = [
+        C.global_head(C.natten((6, 20, 24), (3, 7, 9), (2, 4, 8))),
+        C.global_head(C.natten((1, 48, 60), (1, 11, 11))),
+        C.global_head(C.natten((6, 20, 24), (5, 19, 23), (1, 8, 8))),
+        C.global_head(C.natten((5, 24, 24), (3, 5, 7), (4, 4, 4))),
+        C.global_head(C.natten((3, 30, 32), (1, 1, 1), (1, 4, 16))),
+    ]
+    rep = full_check(ctx, S, 5, 1, None, heads, q, k, v)
+    say(f"  nnz={rep.nnz} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g}")
+
+
 def test_determinism(ctx):
     say("[gpu] determinism")
     from paper_2504_16083_amd import mmi

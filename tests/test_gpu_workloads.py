@@ -152,3 +152,16 @@ def test_qboundary_grid_1m(ctx):
     rep = sampled_check(ctx, wl, q, k, v, [0, 27])
     say(f"  rows={rep.rows} ties={rep.ties} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g} nnz={rep.nnz}")
     assert len(rep.ties) <= 1
+
+
+def test_natten_video(ctx):
+    """Neighborhood attention on the video DiT token grid (118,800 tokens,
+    24 heads, 9 x 15 x 15 windows) in the launch configuration bench.py
+    times: tile permutation and block index bit-exact, O/LSE on sampled
+    rows, two heads."""
+    wl = workloads.natten_video()
+    say(f"[gpu] {wl.name} grid {wl.extra['grid']} tile {wl.extra['tile']}")
+    q, k, v = generate.make_qkv(wl, "cuda")
+    rep = sampled_check(ctx, wl, q, k, v, [0, 23])
+    say(f"  rows={rep.rows} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g} nnz={rep.nnz}")
+    assert not rep.ties
