@@ -156,7 +156,8 @@ typedef struct mmi_head_stats {
   int32_t split_rows;            /* query blocks split across work items */
   int32_t sigma[MMI_MAX_MODALITIES];  /* chosen Grid stride per op slot (0 = not Grid / dense fallback) */
   int32_t phase[MMI_MAX_MODALITIES];
-  int32_t group_stride;          /* query-block stride of the attention row groups (1, 2, 4 or 8) */
+  int32_t group_stride;          /* query-block stride of the attention row groups: 1, 2, 4, 8, or for
+                                    NATTEN heads the tile count of a tile row or of a tile layer */
   int64_t loaded_blocks;         /* key blocks staged for this head (sum of the row-group unions) */
 } mmi_head_stats;
 

@@ -103,6 +103,7 @@ struct HeadDev {
   // member r selects that key block). Member r of group g is query block
   // (g / rho) * R * rho + g % rho + r * rho; rho is chosen per head.
   int32_t gcap;               // capacity of the per-group arrays (>= groups for any stride)
+  int32_t rho_alt[2];         // extra row-stride candidates besides 1, 2, 4, 8 (0 = none)
   int32_t* gp;                // [2] chosen row stride rho of the groups, number of groups
   int32_t* gcount;            // [groups] union sizes
   int32_t* growptr;           // [ngroups+1]
@@ -165,8 +166,10 @@ hipError_t launch_key_summaries(const HeadDev* heads, int nheads, OpDev* ops, in
                                 Groups g, int max_nbk, int max_sel, hipStream_t st);
 hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* ops, Groups g, int max_nbq,
                                hipStream_t st);
-// Chooses each head's row stride rho in {1, 2, 4, 8} (smallest total union,
-// ties to the smaller rho); cand: int64 scratch [nheads][4].
+// Chooses each head's row stride rho among 1, 2, 4, 8 and the head's
+// rho_alt (smallest total union, ties to the earlier candidate); cand: int64
+// scratch [nheads][NRHO].
+constexpr int NRHO = 6;
 hipError_t launch_group_stride(const HeadDev* heads, int nheads, int R, int max_groups, int64_t* cand,
                                hipStream_t st);
 hipError_t launch_group_count(const HeadDev* heads, int nheads, int R, int max_groups, hipStream_t st);

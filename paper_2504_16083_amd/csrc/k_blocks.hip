@@ -350,18 +350,24 @@ __global__ void k_zero64(int64_t* p, int n) {
   if (i < n) p[i] = 0;
 }
 
+// Candidate row strides: 1, 2, 4, 8 and the head's extra ones (0 = none).
+__device__ __forceinline__ int rho_candidate(const HeadDev& hd, int c) {
+  return c < 4 ? 1 << c : hd.rho_alt[c - 4];
+}
+
 __global__ __launch_bounds__(256) void k_group_eval(const HeadDev* heads, int R, int64_t* cand) {
   const HeadDev hd = heads[blockIdx.x];
   const int g = blockIdx.y;
   __shared__ int sh;
-  for (int c = 0; c < 4; ++c) {
-    const int rho = 1 << c;
+  for (int c = 0; c < NRHO; ++c) {
+    const int rho = rho_candidate(hd, c);
+    if (rho <= 0) continue;
     if (g >= groups_for(hd.nbq, R, rho)) continue;      // uniform over the block
     if (threadIdx.x == 0) sh = 0;
     __syncthreads();
     atomicAdd(&sh, union_count(hd, g, R, rho));
     __syncthreads();
-    if (threadIdx.x == 0) atomicAdd(reinterpret_cast<unsigned long long*>(&cand[blockIdx.x * 4 + c]),
+    if (threadIdx.x == 0) atomicAdd(reinterpret_cast<unsigned long long*>(&cand[blockIdx.x * NRHO + c]),
                                     (unsigned long long)sh);
     __syncthreads();
   }
@@ -372,16 +378,16 @@ __global__ void k_group_pick(const HeadDev* heads, int nheads, int R, const int6
   if (h >= nheads) return;
   const HeadDev hd = heads[h];
   int best = 0;
-  for (int c = 1; c < 4; ++c)
-    if (cand[h * 4 + c] < cand[h * 4 + best]) best = c;
-  hd.gp[0] = 1 << best;
-  hd.gp[1] = groups_for(hd.nbq, R, 1 << best);
+  for (int c = 1; c < NRHO; ++c)
+    if (rho_candidate(hd, c) > 0 && cand[h * NRHO + c] < cand[h * NRHO + best]) best = c;
+  hd.gp[0] = rho_candidate(hd, best);
+  hd.gp[1] = groups_for(hd.nbq, R, hd.gp[0]);
 }
 
 hipError_t launch_group_stride(const HeadDev* heads, int nheads, int R, int max_groups, int64_t* cand,
                                hipStream_t st) {
   if (nheads <= 0 || max_groups <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_zero64, dim3((nheads * 4 + 255) / 256), dim3(256), 0, st, cand, nheads * 4);
+  hipLaunchKernelGGL(k_zero64, dim3((nheads * NRHO + 255) / 256), dim3(256), 0, st, cand, nheads * NRHO);
   hipLaunchKernelGGL(k_group_eval, dim3(nheads, max_groups), dim3(256), 0, st, heads, R, cand);
   hipLaunchKernelGGL(k_group_pick, dim3((nheads + 63) / 64), dim3(64), 0, st, heads, nheads, R, cand);
   return hipGetLastError();

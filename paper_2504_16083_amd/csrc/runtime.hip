@@ -689,7 +689,15 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
     hd.counts = dalloc<int32_t>(P, hd.nbq);
     hd.rowptr = dalloc<int32_t>(P, hd.nbq + 1);
     hd.bitmap = dalloc<uint32_t>(P, (size_t)hd.nbq * hd.nwords);
-    hd.gcap = (hd.nbq + R - 1) / R + 8;       // >= groups_for(nbq, R, rho) for rho <= 8
+    if (c.kind == MMI_HEAD_GLOBAL && c.global.kind == MMI_OP_NATTEN) {
+      // neighbouring tiles along h and along t as row-group members
+      const int ntw = (c.global.grid_w + c.global.tile_w - 1) / c.global.tile_w;
+      const int nth = (c.global.grid_h + c.global.tile_h - 1) / c.global.tile_h;
+      hd.rho_alt[0] = ntw > 8 ? ntw : 0;
+      hd.rho_alt[1] = nth * ntw > 8 && nth > 1 ? nth * ntw : 0;
+    }
+    const int max_rho = std::max(8, std::max(hd.rho_alt[0], hd.rho_alt[1]));
+    hd.gcap = (hd.nbq + R - 1) / R + max_rho;   // >= groups_for(nbq, R, rho) for every candidate
     hd.gp = dalloc<int32_t>(P, 2);
     hd.gcount = dalloc<int32_t>(P, hd.gcap);
     hd.growptr = dalloc<int32_t>(P, hd.gcap + 1);
@@ -730,7 +738,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   HIPCHK(launch_key_summaries(P->d_heads, p.Hq, P->d_ops, (int)P->ops.size(), g, max_nbk, bd.max_sel, st));
   const int chunk = ctx->chunk_blocks;
   HIPCHK(launch_blocks_count(P->d_heads, p.Hq, P->d_ops, g, max_nbq, st));
-  int64_t* d_cand = dalloc<int64_t>(P, (size_t)p.Hq * 4);
+  int64_t* d_cand = dalloc<int64_t>(P, (size_t)p.Hq * NRHO);
   HIPCHK(launch_group_stride(P->d_heads, p.Hq, R, max_groups, d_cand, st));
   HIPCHK(launch_group_count(P->d_heads, p.Hq, R, max_groups, st));
   const size_t ntot = (size_t)p.Hq * NTOT;

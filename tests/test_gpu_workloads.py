@@ -49,12 +49,12 @@ def test_workload_parity(ctx, cid, nheads):
     assert len(rep.ties) <= max(1, len(heads) // 4)
 
 
-def _union_totals(plan, h, R=4):
+def _union_totals(plan, h, R=4, strides=(1, 2, 4, 8)):
     """Total union size of the row groups for each stride, from the exported CSR."""
     rp, col = plan.export(h, "row_ptr"), plan.export(h, "col_idx")
     rows = [set(col[rp[i]:rp[i + 1]].tolist()) for i in range(len(rp) - 1)]
     out = {}
-    for rho in (1, 2, 4, 8):
+    for rho in strides:
         ng = (len(rows) + R * rho - 1) // (R * rho) * rho
         members = [[(g // rho) * R * rho + g % rho + r * rho for r in range(R)] for g in range(ng)]
         out[rho] = sum(len(set().union(*[rows[m] for m in mem if m < len(rows)])) for mem in members)
@@ -93,17 +93,20 @@ def test_row_group_stride_choice(ctx):
     say(f"  ties={rep.ties} max|dO|={rep.max_o:.3g}")
 
 
-def expected_union(rp, col, qperm, kperm, S, R, rho, ngroups):
+def expected_union(rp, col, qperm, kperm, S, R, rho, ngroups, causal=True):
     """Row-group unions rebuilt from the exported CSR and permutations: per
     group, ascending key blocks with select bit r (member r lists the block)
     and mask bit r (member r lists it and its largest key position, INT_BIG
-    with padding, exceeds member r's smallest query position)."""
+    with padding, exceeds member r's smallest query position; bidirectional:
+    the block holds padding)."""
     BIG = 0x3FFFFFFF
     nbq = len(rp) - 1
     kp = kperm.reshape(-1, 64)
     kmax = np.where((kp < 0).any(axis=1), BIG, kp.max(axis=1))
     qp = qperm.reshape(-1, 64)
     qmin = np.where(qp >= 0, qp, BIG).min(axis=1)
+    if not causal:
+        qmin = np.full_like(qmin, BIG - 1)
     ptr, ent = [0], []
     for g in range(ngroups):
         rows = [(g // rho) * (R * rho) + g % rho + r * rho for r in range(R)]
@@ -165,3 +168,24 @@ def test_natten_video(ctx):
     rep = sampled_check(ctx, wl, q, k, v, [0, 23])
     say(f"  rows={rep.rows} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g} nnz={rep.nnz}")
     assert not rep.ties
+    # row groups: the stride with the smallest total union among 1, 2, 4, 8, the
+    # tiles of a tile row (10) and of a tile layer (120); unions bit-exact
+    from paper_2504_16083_amd import mmi
+    g, t = wl.extra["grid"], wl.extra["tile"]
+    ntw, nth = -(-g[2] // t[2]), -(-g[1] // t[1])
+    plan = mmi.Plan(ctx, mmi.Problem(wl.S, wl.Hq, wl.Hkv, None), wl.heads, q, k)
+    try:
+        st = plan.stats(0)
+        tot = _union_totals(plan, 0, strides=(1, 2, 4, 8, ntw, nth * ntw))
+        best = min(tot, key=lambda r: (tot[r], [1, 2, 4, 8, ntw, nth * ntw].index(r)))
+        say(f"  stride {st.group_stride}, union totals {tot}")
+        assert st.group_stride == best
+        uptr, uent = plan.export(0, "union_ptr"), plan.export(0, "union")
+        ptr, ent = expected_union(plan.export(0, "row_ptr"), plan.export(0, "col_idx"), plan.export(0, "qperm"),
+                                  plan.export(0, "kperm"), wl.S, 4, st.group_stride, len(uptr) - 1,
+                                  causal=False)
+        assert len(uent) == st.loaded_blocks
+        np.testing.assert_array_equal(uptr, ptr)
+        np.testing.assert_array_equal(uent, ent)
+    finally:
+        plan.destroy()
