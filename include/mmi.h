@@ -253,6 +253,17 @@ int mmi_permute_rows(const void* src, int64_t src_stride, void* dst, int64_t dst
 int mmi_unpermute_rows(const void* src, int64_t src_stride, void* dst, int64_t dst_stride,
                        const int32_t* perm, int64_t n_src, int64_t row_bytes, void* stream);
 
+/* Objective of the modality-aware pattern search (Appendix A, Algorithm 4:
+ * candidates are scored on the attention output): per head and token class,
+ * out[h * n_class + c] = sum over positions x with cls[x] == c of
+ * sum_d (a[x, h, d] - b[x, h, d])^2, differences in fp32, sums in fp64 in a
+ * fixed order (bitwise reproducible). a, b: device bf16 outputs laid out as O
+ * in `prob` (o strides; prob->modality is not read); cls: device uint8 [S],
+ * positions with cls >= n_class are skipped; out: device double [Hq * n_class],
+ * written on `stream`. 1 <= n_class <= MMI_MAX_MODALITIES. */
+int mmi_output_sqerr(const mmi_problem* prob, const void* a, const void* b, const uint8_t* cls,
+                     int32_t n_class, double* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

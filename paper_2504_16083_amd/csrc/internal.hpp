@@ -198,6 +198,9 @@ struct AttnArgs {
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st);
 hipError_t launch_combine(const AttnArgs& a, const SplitRow* splits, int64_t nsplit, hipStream_t st);
+// k_search.hip: out[h * n_class + c] = sum over x with cls[x] == c of |a[x,h] - b[x,h]|^2
+hipError_t launch_sqerr(const void* a, const void* b, int64_t ss, int64_t sh, const uint8_t* cls, int n_class,
+                        int S, int H, double* out, hipStream_t st);
 // k_permute.hip
 hipError_t launch_permute(const void* src, int64_t ss, void* dst, int64_t ds, const int32_t* perm,
                           int64_t n, int64_t row_bytes, int inverse, hipStream_t st);

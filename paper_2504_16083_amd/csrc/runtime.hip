@@ -1138,4 +1138,19 @@ int mmi_unpermute_rows(const void* src, int64_t src_stride, void* dst, int64_t d
   });
 }
 
+int mmi_output_sqerr(const mmi_problem* prob, const void* a, const void* b, const uint8_t* cls, int32_t n_class,
+                     double* out, void* stream) {
+  return guarded([&] {
+    if (!prob) fail(MMI_ERR_INVALID_ARG, "problem is NULL");
+    mmi_problem p = *prob;
+    p.modality = nullptr;          // not read here
+    p = normalise(&p);
+    if (!a || !b || !cls || !out) fail(MMI_ERR_INVALID_ARG, "NULL pointer");
+    if (n_class < 1 || n_class > MMI_MAX_MODALITIES)
+      fail(MMI_ERR_INVALID_ARG, "n_class must be in [1, %d]", MMI_MAX_MODALITIES);
+    aligned16(a, "a"); aligned16(b, "b");
+    HIPCHK(launch_sqerr(a, b, p.o_stride_s, p.o_stride_h, cls, n_class, (int)p.S, p.Hq, out, (hipStream_t)stream));
+  });
+}
+
 }  // extern "C"

@@ -72,7 +72,7 @@ class mmi_plan_timing(ct.Structure):
 SYMBOLS = ["mmi_plan_timing_get", "mmi_version", "mmi_status_str", "mmi_last_error", "mmi_ctx_create", "mmi_ctx_destroy",
            "mmi_plan_create", "mmi_plan_execute", "mmi_plan_stats", "mmi_plan_export",
            "mmi_plan_destroy", "mmi_attention", "mmi_dense_attention", "mmi_permute_rows",
-           "mmi_unpermute_rows"]
+           "mmi_unpermute_rows", "mmi_output_sqerr"]
 
 _lib = None
 
@@ -100,6 +100,7 @@ def lib():
             "mmi_dense_attention": ([vp, ct.POINTER(mmi_problem), vp, vp, vp, vp, vp, vp], i32),
             "mmi_permute_rows": ([vp, i64, vp, i64, vp, i64, i64, vp], i32),
             "mmi_unpermute_rows": ([vp, i64, vp, i64, vp, i64, i64, vp], i32),
+            "mmi_output_sqerr": ([ct.POINTER(mmi_problem), vp, vp, vp, i32, vp, vp], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -297,6 +298,13 @@ def mmi_unpermute_rows(src, dst, perm, stream=None):
     _check(lib().mmi_unpermute_rows(_ptr(src), src.stride(0) * src.element_size(), _ptr(dst),
                                     dst.stride(0) * dst.element_size(), _ptr(perm), perm.numel(), rb,
                                     _stream(stream)))
+
+
+def mmi_output_sqerr(prob, a, b, cls, n_class, out, stream=None):
+    """out[h * n_class + c] (device float64) = squared difference of outputs a
+    and b summed over the positions of class c."""
+    _check(lib().mmi_output_sqerr(ct.byref(prob.c), _ptr(a), _ptr(b), _ptr(cls), int(n_class), _ptr(out),
+                                  _stream(stream)))
 
 
 @atexit.register

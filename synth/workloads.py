@@ -126,6 +126,26 @@ def config4() -> Workload:
                     extra={"text_at_frames": at.tolist()})
 
 
+def search_calibration() -> Workload:
+    """Calibration sample of the pattern search (Appendix C.5: one sample of
+    at most 25K tokens): 24,576 tokens, T V T V with text U{512..2048} and
+    whole 196-token frames, 28/4 heads, the 128K workload's planted
+    structure."""
+    rng = _rng(6)
+    S, F = 24576, 196
+    text = [int(rng.integers(512, 2049)) for _ in range(2)]
+    nf = (S - sum(text)) // F
+    text[-1] += S - sum(text) - nf * F
+    cut = int(rng.integers(nf // 4, 3 * nf // 4))
+    segs = [(0, text[0]), (1, cut * F), (0, text[1]), (1, (nf - cut) * F)]
+    mod = _layout(segs)
+    assert len(mod) == S
+    st = Structure(sigma=[F] * 4, amp=2.0, text_amp=1.0)
+    st.line_slot = _line_slots(rng, st.sigma)
+    heads = [C.global_head(C.dense())] * 28
+    return Workload("search_calib_24k", S, 28, 4, mod, heads, st, SEED0 + 6, frame=F)
+
+
 def natten_video() -> Workload:
     """Neighborhood attention stand-in for one video DiT layer (Appendix F):
     a 33 x 45 x 80 token grid (118,800 tokens: the latent of a 129-frame
