@@ -156,6 +156,48 @@ def test_natten(ctx):
     say(f"  nnz={rep.nnz} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g}")
 
 
+@pytest.mark.parametrize("S", [1, 2, 63, 64, 65, 127])
+def test_tiny_sequences(ctx, S):
+    """Sequences of one token to two blocks, every global op kind (a Grid
+    search with too few tokens falls back to dense; 1-token windows)."""
+    say(f"[gpu] tiny S={S}")
+    q, k, v = _rand_qkv(S, 8, 2, seed=100 + S)
+    heads = [C.global_head(C.dense()), C.global_head(C.ashape(1, 4)), C.global_head(C.vslash(3, 2)),
+             C.global_head(C.grid(1, 8)), C.global_head(C.trishape(1, 3, 2)), C.global_head(C.sf_fixed(5, 3)),
+             C.global_head(C.sf_strided(2, 7)),
+             C.global_head(C.natten((1, 1, S), (1, 1, 1 if S < 3 else 3), (1, 1, 64)))]
+    rep = full_check(ctx, S, 8, 2, None, heads, q, k, v)
+    say(f"  nnz={rep.nnz} max|dO|={rep.max_o:.3g}")
+
+
+def test_eight_modalities(ctx):
+    """Eight modalities in short interleaved segments (1-89 tokens, most
+    groups below one block): Q-Boundary heads with a different op per
+    modality (two Grid modalities: three key layouts) and 2D-Boundary heads
+    with none / dense / VERT cross pairs."""
+    say("[gpu] eight modalities")
+    S = 700
+    rng = np.random.default_rng(8)
+    mod = np.zeros(S, np.uint8)
+    pos, m = 0, 0
+    while pos < S:
+        n = int(rng.integers(1, 90))
+        mod[pos:pos + n] = m
+        pos += n
+        m = (m + 1) % 8
+    q, k, v = _rand_qkv(S, 4, 2, seed=21)
+    ops = [C.dense(), C.ashape(4, 40), C.vslash(6, 5), C.grid(3, 12), C.trishape(2, 30, 10), C.sf_fixed(20, 9),
+           C.sf_strided(16, 5), C.grid(8, 8, True, False, True)]
+    cross = {(a, b): [C.none(), C.dense(), C.vert(7)][(a + b) % 3] for a in range(8) for b in range(8) if a != b}
+    heads = [C.qboundary_head({m: ops[m] for m in range(8)}),
+             C.boundary2d_head({m: ops[(m + 3) % 8] for m in range(8)}, cross),
+             C.qboundary_head({m: ops[(m + 5) % 8] for m in range(8)}),
+             C.boundary2d_head({m: ops[(m + 1) % 8] for m in range(8)},
+                               {ab: C.vert(3) for ab in cross})]
+    rep = full_check(ctx, S, 4, 2, mod, heads, q, k, v)
+    say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
+
+
 def test_determinism(ctx):
     say("[gpu] determinism")
     from paper_2504_16083_amd import mmi
