@@ -928,6 +928,8 @@ int mmi_plan_create(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* c
         (void)hipStreamSynchronize((hipStream_t)stream);
         free_plan_buffers(P);
       }
+      for (auto& e : P->ev)
+        if (e) (void)hipEventDestroy(e);
       delete P;
     }
     return rc;

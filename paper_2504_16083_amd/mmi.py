@@ -143,16 +143,26 @@ def op_struct(op: C.Op) -> mmi_op:
                   int(op.use_h), int(op.use_v), int(op.use_s), op.bottom, *op.grid, *op.win, *op.tile)
 
 
+def _head_cfg(h) -> mmi_head_cfg:
+    c = mmi_head_cfg()                 # zero-filled: every op not set below is MMI_OP_NONE
+    c.kind = h.kind
+    c.global_ = op_struct(h.op)
+    for m in range(MAXM):
+        c.intra[m] = op_struct(h.intra_op(m))
+    for (mq, mk), op in h.cross.items():
+        c.cross[mq][mk] = op_struct(op)
+    return c
+
+
 def head_cfgs(heads) -> ct.Array:
+    """mmi_head_cfg array for the heads (a config object repeated over heads
+    is marshalled once)."""
     arr = (mmi_head_cfg * len(heads))()
+    done = {}
     for i, h in enumerate(heads):
-        c = arr[i]
-        c.kind = h.kind
-        c.global_ = op_struct(h.op)
-        for m in range(MAXM):
-            c.intra[m] = op_struct(h.intra_op(m))
-            for mk in range(MAXM):
-                c.cross[m][mk] = op_struct(h.cross_op(m, mk))
+        if id(h) not in done:
+            done[id(h)] = _head_cfg(h)
+        arr[i] = done[id(h)]
     return arr
 
 

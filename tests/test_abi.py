@@ -102,3 +102,25 @@ def test_stats_struct_matches_header():
     assert mmi.mmi_head_stats.group_stride.offset == 100
     assert mmi.mmi_head_stats.loaded_blocks.offset == 104
     assert ct.sizeof(mmi.mmi_head_stats) == 112
+
+
+def test_head_cfg_marshalling_fills_every_op():
+    """head_cfgs (a repeated config marshalled once, cross pairs only where
+    set) writes the same bytes as filling every op of every head."""
+    from synth import workloads
+
+    def full(heads):
+        arr = (mmi.mmi_head_cfg * len(heads))()
+        for i, h in enumerate(heads):
+            c = arr[i]
+            c.kind = h.kind
+            c.global_ = mmi.op_struct(h.op)
+            for m in range(mmi.MAXM):
+                c.intra[m] = mmi.op_struct(h.intra_op(m))
+                for mk in range(mmi.MAXM):
+                    c.cross[m][mk] = mmi.op_struct(h.cross_op(m, mk))
+        return arr
+
+    for cid in (2, 4):
+        heads = workloads.by_id(cid).heads
+        assert bytes(mmi.head_cfgs(heads)) == bytes(full(heads))
