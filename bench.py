@@ -39,6 +39,19 @@ TRAFFIC = {
 }
 
 
+def pattern_head(pattern: str, tpf: int):
+    """One head configuration for every head: the paper's baselines with the
+    hyperparameters of its baseline table (tpf = tokens per frame), or
+    Q-Boundary heads with A-shape text and Grid video."""
+    from synth import config as C
+    return {"ashape": C.global_head(C.ashape(128, 4096)),
+            "trishape": C.global_head(C.trishape(128, 4096, 128)),
+            "sf_fixed": C.global_head(C.sf_fixed(tpf, tpf)),
+            "sf_strided": C.global_head(C.sf_strided(tpf, tpf)),
+            "vslash": C.global_head(C.vslash(1000, 1024)),
+            "qb_grid": C.qboundary_head({0: C.ashape(128, 4096), 1: C.grid_window(tpf)})}[pattern]
+
+
 def attention_traffic(workload: str):
     import hashlib
     src = os.path.join(ROOT, "paper_2504_16083_amd", "csrc", "k_attention.hip")
@@ -202,15 +215,7 @@ def main():
 
     wl = workloads.natten_video() if args.workload == "natten" else workloads.by_id(args.config)
     if args.pattern != "method":
-        from synth import config as C
-        tpf = wl.frame or 256        # tokens per frame
-        head = {"ashape": C.global_head(C.ashape(128, 4096)),
-                "trishape": C.global_head(C.trishape(128, 4096, 128)),
-                "sf_fixed": C.global_head(C.sf_fixed(tpf, tpf)),
-                "sf_strided": C.global_head(C.sf_strided(tpf, tpf)),
-                "vslash": C.global_head(C.vslash(1000, 1024)),
-                "qb_grid": C.qboundary_head({0: C.ashape(128, 4096), 1: C.grid_window(tpf)})}[args.pattern]
-        wl.heads = [head] * wl.Hq
+        wl.heads = [pattern_head(args.pattern, wl.frame or 256)] * wl.Hq
         wl.name = f"{wl.name}+{args.pattern}"
     torch.cuda.set_device(0)
     log(f"workload {wl.name}: S={wl.S} Hq={wl.Hq} Hkv={wl.Hkv}")

@@ -29,3 +29,21 @@ def test_workload_layouts_match_sequence_length():
     for cid in range(5):
         wl = workloads.by_id(cid)
         assert len(wl.modality) == wl.S and wl.Hq % wl.Hkv == 0 and len(wl.heads) == wl.Hq
+
+
+def test_bench_baselines_follow_the_printed_table():
+    """bench.py --pattern uses the baseline hyperparameters the paper prints
+    (Appendix, Table 'impl_details'); MInference takes its smallest sizes."""
+    import bench
+    t = json.load(open(os.path.join(HERE, "golden", "baselines.json")))
+    tpf = 196
+    op = bench.pattern_head("ashape", tpf).op
+    assert (op.sink, op.local) == (t["ashape"]["sink"], t["ashape"]["local"])
+    op = bench.pattern_head("trishape", tpf).op
+    assert (op.sink, op.local, op.bottom) == (t["trishape"]["sink"], t["trishape"]["local"], t["trishape"]["bottom"])
+    for name in ("sf_fixed", "sf_strided"):
+        op = bench.pattern_head(name, tpf).op
+        assert t[name] == {"local": "token_per_frame", "vline_stride": "token_per_frame"}
+        assert (op.local, op.stride_lo) == (tpf, tpf)
+    op = bench.pattern_head("vslash", tpf).op
+    assert (op.n_vertical, op.n_slash) == (min(t["minference"]["vertical_size"]), min(t["minference"]["slash_size"]))
