@@ -217,6 +217,57 @@ def test_determinism(ctx):
     assert np.array_equal(outs[0][2], outs[1][2]) and np.array_equal(outs[0][3], outs[1][3])
 
 
+def test_side_stream_and_one_shot(ctx):
+    """A plan created and executed on a side stream, the one-shot entry point
+    and the default-stream plan give bitwise the same output; a plan executes
+    twice with the same result; strided (non-packed) Q/K/V views give the
+    same output as packed copies."""
+    from paper_2504_16083_amd import mmi
+    say("[gpu] side stream / one-shot / strides")
+    wl = workloads.config2()
+    S = 16384
+    mod = wl.modality[:S].copy()
+    heads = wl.heads[:8]
+    q, k, v = _rand_qkv(S, 8, 2, seed=31, scale_k=2.0)
+    prob = mmi.Problem(S, 8, 2, mod)
+    ref = torch.empty_like(q)
+    plan = mmi.Plan(ctx, prob, heads, q, k)
+    plan.execute(q, k, v, ref)
+    again = torch.empty_like(q)
+    plan.execute(q, k, v, again)
+    torch.cuda.synchronize()
+    plan.destroy()
+    assert torch.equal(ref, again)
+    side = torch.cuda.Stream()
+    o2 = torch.empty_like(q)
+    with torch.cuda.stream(side):
+        p2 = mmi.Plan(ctx, prob, heads, q, k, side)
+        p2.execute(q, k, v, o2, None, side)
+    side.synchronize()
+    p2.destroy()
+    assert torch.equal(ref, o2)
+    o3 = torch.empty_like(q)
+    mmi.mmi_attention(ctx, prob, heads, q, k, v, o3)
+    torch.cuda.synchronize()
+    assert torch.equal(ref, o3)
+    # Q/K/V as views into wider buffers (token stride larger than H*128)
+    big_q = torch.zeros(S, 10, 128, dtype=q.dtype, device="cuda")
+    big_k = torch.zeros(S, 3, 128, dtype=k.dtype, device="cuda")
+    big_v = torch.zeros(S, 3, 128, dtype=v.dtype, device="cuda")
+    big_q[:, 1:9] = q
+    big_k[:, :2] = k
+    big_v[:, 1:3] = v
+    qs, ks, vs = big_q[:, 1:9], big_k[:, :2], big_v[:, 1:3]
+    probs = mmi.Problem(S, 8, 2, mod, strides={n: (t.stride(0), t.stride(1)) for n, t in
+                                                (("q", qs), ("k", ks), ("v", vs))})
+    o4 = torch.empty_like(q)
+    p4 = mmi.Plan(ctx, probs, heads, qs, ks)
+    p4.execute(qs, ks, vs, o4)
+    torch.cuda.synchronize()
+    p4.destroy()
+    assert torch.equal(ref, o4)
+
+
 def test_permute_roundtrip(ctx):
     say("[gpu] permute/unpermute")
     from paper_2504_16083_amd import mmi
