@@ -159,6 +159,11 @@ typedef struct mmi_head_stats {
   int32_t group_stride;          /* query-block stride of the attention row groups: 1, 2, 4, 8, or for
                                     NATTEN heads the tile count of a tile row or of a tile layer */
   int64_t loaded_blocks;         /* key blocks staged for this head (sum of the row-group unions) */
+  int64_t blocks_by_modality[MMI_MAX_MODALITIES][MMI_MAX_MODALITIES];
+  /* selected blocks by [query modality][key modality], a block taking the modality of its
+     first token (the selected-block cost per modality and per modality pair that the pattern
+     search budgets; query and key blocks are modality-pure in 2D-Boundary heads, query blocks
+     in Q-Boundary heads) */
 } mmi_head_stats;
 
 /* Stage durations of a plan, from HIP events recorded on the plan's stream

@@ -159,6 +159,7 @@ struct mmi_plan {
   int64_t nitems = 0, nsplit = 0, nparts = 0;
   int R = 1;                      // query blocks per attention work item
   int32_t* d_tpos = nullptr;
+  std::vector<uint8_t> mod;       // host modality of every position (all 0 without a layout)
   std::vector<float*> est_lse2;  // per rowset
   std::vector<std::vector<uint8_t>> keep;   // host sources of asynchronous uploads
   hipEvent_t ev[7] = {};          // stage boundaries: create 0..3, execute 4..6
@@ -481,6 +482,8 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   P->stream = st;
   P->prob = p;
   P->prob.modality = nullptr;
+  P->mod.assign((size_t)p.S, 0);
+  if (p.modality) std::copy(p.modality, p.modality + p.S, P->mod.begin());
   P->S = (int)p.S; P->Hq = p.Hq; P->Hkv = p.Hkv;
   const int S = P->S, G = p.Hq / p.Hkv;
   Builder bd{P};
@@ -989,6 +992,26 @@ int mmi_plan_stats(mmi_plan* P, int head, mmi_head_stats* out) {
     HIPCHK(hipMemcpy(gp, hd.gp, sizeof gp, hipMemcpyDeviceToHost));
     s.group_stride = gp[0];
     s.loaded_blocks = H.gnnz;
+    // selected blocks by (query modality, key modality), from the block index
+    auto block_mods = [&](const int32_t* perm, int nblk) {
+      std::vector<int32_t> slots((size_t)nblk * B);
+      if (perm) HIPCHK(hipMemcpy(slots.data(), perm, slots.size() * 4, hipMemcpyDeviceToHost));
+      else for (size_t x = 0; x < slots.size(); ++x) slots[x] = x < (size_t)P->S ? (int32_t)x : -1;
+      std::vector<int> m(nblk, -1);
+      for (int j = 0; j < nblk; ++j)
+        for (int x = 0; x < B && m[j] < 0; ++x)
+          if (slots[(size_t)j * B + x] >= 0) m[j] = P->mod[slots[(size_t)j * B + x]];
+      return m;
+    };
+    const std::vector<int> qm = block_mods(hd.qperm, hd.nbq), km = block_mods(hd.kperm, hd.nbk);
+    std::vector<int32_t> rp(hd.nbq + 1), col(std::max<int64_t>(H.nnz, 1));
+    HIPCHK(hipMemcpy(rp.data(), hd.rowptr, rp.size() * 4, hipMemcpyDeviceToHost));
+    if (H.nnz) HIPCHK(hipMemcpy(col.data(), hd.col, (size_t)H.nnz * 4, hipMemcpyDeviceToHost));
+    for (int i = 0; i < hd.nbq; ++i) {
+      if (qm[i] < 0) continue;
+      for (int e = rp[i]; e < rp[i + 1]; ++e)
+        if (km[col[e]] >= 0) ++s.blocks_by_modality[qm[i]][km[col[e]]];
+    }
     *out = s;
   });
 }

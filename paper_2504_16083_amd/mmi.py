@@ -60,7 +60,7 @@ class mmi_head_stats(ct.Structure):
     _fields_ = [("kind", ct.c_int32), ("n_qblocks", ct.c_int32), ("n_kblocks", ct.c_int32),
                 ("nnz_blocks", ct.c_int64), ("causal_blocks", ct.c_int64), ("split_rows", ct.c_int32),
                 ("sigma", ct.c_int32 * MAXM), ("phase", ct.c_int32 * MAXM), ("group_stride", ct.c_int32),
-                ("loaded_blocks", ct.c_int64)]
+                ("loaded_blocks", ct.c_int64), ("blocks_by_modality", (ct.c_int64 * MAXM) * MAXM)]
 
 
 class mmi_plan_timing(ct.Structure):

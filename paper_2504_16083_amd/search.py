@@ -74,13 +74,10 @@ class _Runner:
         self.err_out = torch.empty(Hq * len(self.mods), dtype=torch.float64, device=q.device)
         self.plans = 0
 
-    def _block_mod(self, perm):
-        blk = perm.reshape(-1, 64)
-        first = np.where(blk >= 0, blk, np.iinfo(np.int32).max).min(axis=1)
-        return np.where(first < self.S, self.mod[np.minimum(first, self.S - 1)], 255)
-
-    def run(self, heads, pairs=False):
-        """-> (O, costs): costs[h] = {"all": n, m: n, ("pair", a, b): n (if pairs)}."""
+    def run(self, heads):
+        """-> (O, costs): costs[h] = {"all": n, m: n, ("pair", a, b): n}, the
+        selected blocks of the head, of modality m's query blocks, and of m's
+        query blocks against b's key blocks (from the plan's statistics)."""
         plan = mmi.Plan(self.ctx, self.prob, heads, self.q, self.k, self.stream)
         o = torch.empty_like(self.q)
         plan.execute(self.q, self.k, self.v, o, None, self.stream)
@@ -88,20 +85,13 @@ class _Runner:
         costs = []
         try:
             for h in range(self.Hq):
-                rp = plan.export(h, "row_ptr").astype(np.int64)
-                per = np.diff(rp)
-                qm = self._block_mod(plan.export(h, "qperm"))
-                c = {"all": int(per.sum())}
-                for m in self.mods:
-                    c[m] = int(per[qm == m].sum())
-                if pairs:
-                    col = plan.export(h, "col_idx")
-                    km = self._block_mod(plan.export(h, "kperm"))[col]
-                    rows = np.repeat(qm, per)
-                    for a in self.mods:
-                        for b in self.mods:
-                            if a != b:
-                                c[("pair", a, b)] = int(((rows == a) & (km == b)).sum())
+                st = plan.stats(h)
+                bm = st.blocks_by_modality
+                c = {"all": int(st.nnz_blocks)}
+                for a in self.mods:
+                    c[a] = sum(int(bm[a][b]) for b in range(mmi.MAXM))
+                    for b in self.mods:
+                        c[("pair", a, b)] = int(bm[a][b])
                 costs.append(c)
         finally:
             plan.destroy()
@@ -173,7 +163,7 @@ def search(ctx, S, Hq, Hkv, modality, q, k, v, cands, xc, target, stream=None):
                 for ai, a in enumerate(mods):
                     cross[(a, mods[(ai + kk) % n])] = op
                 heads.append(C.boundary2d_head(intra[h], cross))
-            o, cc = R.run(heads, pairs=True)
+            o, cc = R.run(heads)
             ee = R.sqerr(o, ref)
             for h in range(Hq):
                 cost = {a: cc[h][("pair", a, mods[(ai + kk) % n])] for ai, a in enumerate(mods)}

@@ -101,7 +101,8 @@ def test_stats_struct_matches_header():
     # kind, n_qblocks, n_kblocks (12) + pad (4) + 2 x int64 (16) + split_rows (4) + 2 x 8 int32 (64)
     assert mmi.mmi_head_stats.group_stride.offset == 100
     assert mmi.mmi_head_stats.loaded_blocks.offset == 104
-    assert ct.sizeof(mmi.mmi_head_stats) == 112
+    assert mmi.mmi_head_stats.blocks_by_modality.offset == 112
+    assert ct.sizeof(mmi.mmi_head_stats) == 112 + 64 * 8
 
 
 def test_head_cfg_marshalling_fills_every_op():
