@@ -193,10 +193,11 @@ typedef struct mmi_plan_timing {
 #define MMI_EXPORT_PARAMS 9      /* int32[4]: {sigma, phase, L_c, n_rows} (sigma 0 = dense) */
 #define MMI_EXPORT_EST_LSE 10    /* float[n_rows]: natural-log LSE of the estimation rows */
 #define MMI_EXPORT_UNION_PTR 11  /* int32[n_groups+1]: entry offsets of the attention row groups */
-#define MMI_EXPORT_UNION 12      /* int32[loaded_blocks]: row-group union entries, ascending key block
-                                    per group: key block | select bits << 16 | mask bits << 24 (bit r:
-                                    member r selects the block / the block holds a key position above
-                                    member r's smallest query position, or padding) */
+#define MMI_EXPORT_UNION 12      /* int32[loaded_blocks]: row-group union entries, per group the key
+                                    blocks every member selects, then the others, each ascending:
+                                    key block | select bits << 16 | mask bits << 24 (bit r: member r
+                                    selects the block / the block holds a key position above member
+                                    r's smallest query position, or padding) */
 
 int mmi_version(void);
 const char* mmi_status_str(int status);   /* static string, never NULL */

@@ -12,7 +12,7 @@
 //   threshold tests, slash offsets), then stores the bitmap and its
 //   popcount. Bit setting is an OR, so the result is order independent.
 // k_group_count / k_group_fill: the union of the key-block sets of R
-//   consecutive query blocks, with a per-query-block flag on every entry
+//   query blocks (a row group), with a per-query-block flag on every entry
 //   (the attention kernel loads each key block once for all R query blocks).
 // k_blocks_scan: per head, prefix sums of counts (CSR row pointers), of the
 //   group unions and of work-item counts.
@@ -521,7 +521,10 @@ __global__ __launch_bounds__(256) void k_blocks_fill(const HeadDev* heads) {
   }
 }
 
-// Union entries of a row group, ascending in the key block: key block in
+// Union entries of a row group: first the key blocks every member selects,
+// then the others, each part ascending (row groups running side by side then
+// start on the blocks they most likely share, which measured ~2% faster than
+// one ascending list at 1M tokens). Key block in
 // bits 0-15, bit 16+r set if query block r of the group selects it, bit 24+r
 // set if it does and the key block holds a position above the smallest
 // query position of query block r (or padding), i.e. needs the causal mask
@@ -546,29 +549,37 @@ __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R)
   }
   const int per = (hd.nwords + 255) / 256;
   const int w0 = threadIdx.x * per;
-  int cnt = 0;
+  int cntA = 0, cntB = 0;        // entries every member selects / the others
   for (int w = w0; w < min(w0 + per, hd.nwords); ++w) {
-    uint32_t u = 0;
+    uint32_t u = 0, a = 0xffffffffu;
     for (int r = 0; r < R; ++r)
-      if (rows[r] < hd.nbq) u |= hd.bitmap[(int64_t)rows[r] * hd.nwords + w];
-    cnt += __popc(u);
+      if (rows[r] < hd.nbq) { const uint32_t x = hd.bitmap[(int64_t)rows[r] * hd.nwords + w]; u |= x; a &= x; }
+    a &= u;
+    cntA += __popc(a);
+    cntB += __popc(u & ~a);
   }
-  buf[threadIdx.x] = cnt;
+  __shared__ int bufB[256];
+  buf[threadIdx.x] = cntA;
+  bufB[threadIdx.x] = cntB;
   __syncthreads();
   for (int off = 1; off < 256; off <<= 1) {
     const int t = threadIdx.x >= off ? buf[threadIdx.x - off] : 0;
+    const int tb = threadIdx.x >= off ? bufB[threadIdx.x - off] : 0;
     __syncthreads();
     buf[threadIdx.x] += t;
+    bufB[threadIdx.x] += tb;
     __syncthreads();
   }
-  int pos = hd.growptr[gr] + buf[threadIdx.x] - cnt;
+  int posA = hd.growptr[gr] + buf[threadIdx.x] - cntA;
+  int posB = hd.growptr[gr] + buf[255] + bufB[threadIdx.x] - cntB;
   for (int w = w0; w < min(w0 + per, hd.nwords); ++w) {
     uint32_t bits[4] = {0, 0, 0, 0};
-    uint32_t u = 0;
+    uint32_t u = 0, a = 0xffffffffu;
     for (int r = 0; r < R; ++r) {
-      if (rows[r] < hd.nbq) bits[r] = hd.bitmap[(int64_t)rows[r] * hd.nwords + w];
+      if (rows[r] < hd.nbq) { bits[r] = hd.bitmap[(int64_t)rows[r] * hd.nwords + w]; a &= bits[r]; }
       u |= bits[r];
     }
+    a &= u;
     while (u) {
       const int b = __ffs(u) - 1;
       const int j = w * 32 + b;
@@ -581,7 +592,8 @@ __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R)
         flags |= sel << (16 + r);
         if (sel && kmax > qmin[r]) flags |= 1u << (24 + r);
       }
-      hd.gcol[pos++] = (int32_t)((uint32_t)j | flags);
+      const int32_t e = (int32_t)((uint32_t)j | flags);
+      if ((a >> b) & 1u) hd.gcol[posA++] = e; else hd.gcol[posB++] = e;
       u &= u - 1;
     }
   }

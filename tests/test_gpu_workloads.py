@@ -95,10 +95,11 @@ def test_row_group_stride_choice(ctx):
 
 def expected_union(rp, col, qperm, kperm, S, R, rho, ngroups, causal=True):
     """Row-group unions rebuilt from the exported CSR and permutations: per
-    group, ascending key blocks with select bit r (member r lists the block)
-    and mask bit r (member r lists it and its largest key position, INT_BIG
-    with padding, exceeds member r's smallest query position; bidirectional:
-    the block holds padding)."""
+    group, the key blocks every (existing) member lists, then the others,
+    each part ascending, with select bit r (member r lists the block) and
+    mask bit r (member r lists it and its largest key position, INT_BIG with
+    padding, exceeds member r's smallest query position; bidirectional: the
+    block holds padding)."""
     BIG = 0x3FFFFFFF
     nbq = len(rp) - 1
     kp = kperm.reshape(-1, 64)
@@ -111,7 +112,10 @@ def expected_union(rp, col, qperm, kperm, S, R, rho, ngroups, causal=True):
     for g in range(ngroups):
         rows = [(g // rho) * (R * rho) + g % rho + r * rho for r in range(R)]
         lists = [set(col[rp[i]:rp[i + 1]].tolist()) if i < nbq else set() for i in rows]
-        for j in sorted(set().union(*lists)):
+        exist = [lists[r] for r in range(R) if rows[r] < nbq]
+        common = set.intersection(*exist) if exist else set()
+        union = set().union(*lists)
+        for j in sorted(common) + sorted(union - common):
             sel = sum(1 << r for r in range(R) if j in lists[r])
             msk = sum(1 << r for r in range(R) if j in lists[r] and kmax[j] > qmin[rows[r]])
             ent.append(np.uint32(j | (sel << 16) | (msk << 24)).view(np.int32))
