@@ -66,6 +66,8 @@ def run_gpu(ctx, S, Hq, Hkv, modality, heads, q, k, v):
 def _rel_err(gpu, ref):
     ref = np.asarray(ref, dtype=np.float64)
     gpu = np.asarray(gpu, dtype=np.float64)
+    if ref.size == 0:
+        return 0.0
     big = np.abs(ref) >= 1e-6 * max(np.abs(ref).max(), 1e-300)
     if not big.any():
         return 0.0
@@ -79,6 +81,10 @@ def compare_head(plan, h, hp: OP.HeadPlan, rep: Report, exact_choices=True):
         s = slot_of(key)
         gv = plan.export(h, "v", s)
         assert len(gv) == est.L_c, (h, key, len(gv), est.L_c)
+        if est.L_c == 0:
+            # a cross pair whose key modality has no token before the final
+            # query rows: nothing to select, the library runs no estimation
+            continue
         ev = _rel_err(gv, est.v)
         assert ev <= SCORE_RTOL, f"head {h} {key}: v rel err {ev}"
         if est.u is not None and hp.ops[key].op.kind == C.OP_VSLASH:

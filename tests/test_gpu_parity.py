@@ -306,3 +306,24 @@ def test_row_group_variants(R, monkeypatch):
         say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
     finally:
         c.close()
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_configs(ctx, seed):
+    """Seeded random layouts (1-4 modalities, segments of any length) and
+    random heads of every kind and op (global ops incl. Grid and
+    neighborhood attention, Q-Boundary incl. Grid modalities, 2D-Boundary
+    with every cross kind) at random lengths up to 5000 tokens."""
+    from random_cfg import random_head, random_layout
+    rng = np.random.default_rng(1000 + seed)
+    S = int(rng.integers(1, 5000))
+    nmod = int(rng.integers(1, 5))
+    mod = random_layout(rng, S, nmod) if nmod > 1 else None
+    mods = sorted(set(mod.tolist())) if mod is not None else [0]
+    heads = [random_head(rng, S, mods) for _ in range(4)]
+    say(f"[gpu] random seed {seed}: S={S} modalities {mods} kinds {[h.kind for h in heads]}")
+    q, k, v = _rand_qkv(S, 4, 2, seed=2000 + seed, scale_k=1.5)
+    rows = None if S <= 2000 else np.unique(np.concatenate(
+        [np.arange(S - 64, S), np.random.default_rng(seed).choice(S, 512, replace=False)]))
+    rep = full_check(ctx, S, 4, 2, mod, heads, q, k, v, rows=rows)
+    say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
