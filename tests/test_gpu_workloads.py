@@ -193,3 +193,23 @@ def test_natten_video(ctx):
         np.testing.assert_array_equal(uent, ent)
     finally:
         plan.destroy()
+
+
+def test_max_sequence_length(ctx):
+    """The largest supported length, S = 2^21 (2,097,152 tokens): A-shape and
+    Grid heads on a text + video layout with 256-token frames, block index
+    bit-exact and O/LSE on sampled rows (one head per oracle pass, about a
+    minute each on the host)."""
+    S, F = 1 << 21, 256
+    mod = np.ones(S, np.uint8)
+    mod[:512] = 0
+    st = Structure(sigma=[F], amp=2.0, text_amp=1.0)
+    st.line_slot = [200]
+    heads = [C.global_head(C.ashape(128, 4096)), C.global_head(C.grid_window(F))]
+    wl = Workload("max_2m", S, 2, 1, mod, heads, st, 20250416 + 21, frame=F)
+    q, k, v = generate.make_qkv(wl, "cuda")
+    for h in (0, 1):
+        say(f"[gpu] S = {S}, head {h}")
+        rep = sampled_check(ctx, wl, q, k, v, [h])
+        say(f"  rows={rep.rows} ties={rep.ties} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g} nnz={rep.nnz}")
+        assert not rep.ties
