@@ -49,6 +49,7 @@ def pattern_head(pattern: str, tpf: int):
             "sf_fixed": C.global_head(C.sf_fixed(tpf, tpf)),
             "sf_strided": C.global_head(C.sf_strided(tpf, tpf)),
             "vslash": C.global_head(C.vslash(1000, 1024)),
+            "grid": C.global_head(C.grid_window(tpf)),
             "qb_grid": C.qboundary_head({0: C.ashape(128, 4096), 1: C.grid_window(tpf)})}[pattern]
 
 
@@ -82,10 +83,11 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8)
     ap.add_argument("--pattern", default="method",
-                    choices=["method", "ashape", "trishape", "sf_fixed", "sf_strided", "vslash", "qb_grid"],
+                    choices=["method", "ashape", "trishape", "sf_fixed", "sf_strided", "vslash", "grid", "qb_grid"],
                     help="every head on one pattern instead of the workload's per-head patterns: one of "
-                         "the paper's baselines (Section 4.1, baseline hyperparameter table), or qb_grid "
-                         "(Q-Boundary heads, A-shape text and Grid video)")
+                         "the paper's baselines (Section 4.1, baseline hyperparameter table), grid (Grid "
+                         "heads, strides within 8 of the frame size), or qb_grid (Q-Boundary heads, A-shape "
+                         "text and Grid video)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain copy of this many MiB (k_permute, identity) before the steps, "
                          "as the reference dispatch for HBM byte counters")
