@@ -361,7 +361,7 @@ __device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, cons
       const int j = i - NQ, stp = j >> 2, dt = j & 3;
       ws.o[dt] = mfma32(av, p_cur[stp], ws.o[dt]);
     }
-    const int pe = (i + 1) * SM_PIECES / NM;
+    const int pe = (i + 1) * SM_PIECES / (NM > 0 ? NM : 1);
 #pragma unroll
     for (; pc < pe; ++pc) softmax_piece(pc, s_sm, sc, ws.m, ws.l, p_new, alpha, st);
   }

@@ -505,7 +505,7 @@ __global__ __launch_bounds__(256) void k_blocks_fill(const HeadDev* heads) {
   buf[threadIdx.x] = cnt;
   __syncthreads();
   for (int off = 1; off < 256; off <<= 1) {
-    const int t = threadIdx.x >= off ? buf[threadIdx.x - off] : 0;
+    const int t = (int)threadIdx.x >= off ? buf[threadIdx.x - off] : 0;
     __syncthreads();
     buf[threadIdx.x] += t;
     __syncthreads();
@@ -563,8 +563,8 @@ __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R)
   bufB[threadIdx.x] = cntB;
   __syncthreads();
   for (int off = 1; off < 256; off <<= 1) {
-    const int t = threadIdx.x >= off ? buf[threadIdx.x - off] : 0;
-    const int tb = threadIdx.x >= off ? bufB[threadIdx.x - off] : 0;
+    const int t = (int)threadIdx.x >= off ? buf[threadIdx.x - off] : 0;
+    const int tb = (int)threadIdx.x >= off ? bufB[threadIdx.x - off] : 0;
     __syncthreads();
     buf[threadIdx.x] += t;
     bufB[threadIdx.x] += tb;

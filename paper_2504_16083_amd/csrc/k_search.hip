@@ -43,7 +43,7 @@ __global__ __launch_bounds__(SQ_THREADS) void k_sqerr(const uint16_t* a, const u
     if (lane == 0) part[wave][k] = v;
   }
   __syncthreads();
-  if (threadIdx.x < n_class) {
+  if ((int)threadIdx.x < n_class) {
     double s = 0.0;
     for (int w = 0; w < SQ_THREADS / 64; ++w) s += part[w][threadIdx.x];
     out[(int64_t)h * n_class + threadIdx.x] = s;

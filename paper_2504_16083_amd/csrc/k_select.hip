@@ -45,7 +45,7 @@ __global__ __launch_bounds__(256) void k_grid_fold(const GridJob* jobs) {
   bp[threadIdx.x] = bestp;
   __syncthreads();
   for (int w = 128; w > 0; w >>= 1) {
-    if (threadIdx.x < w) {
+    if ((int)threadIdx.x < w) {
       const float ov = bv[threadIdx.x + w];
       const int op = bp[threadIdx.x + w];
       if (ov > bv[threadIdx.x] || (ov == bv[threadIdx.x] && op < bp[threadIdx.x])) {

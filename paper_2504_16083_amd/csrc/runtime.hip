@@ -486,7 +486,8 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   if (p.modality) std::copy(p.modality, p.modality + p.S, P->mod.begin());
   P->S = (int)p.S; P->Hq = p.Hq; P->Hkv = p.Hkv;
   const int S = P->S, G = p.Hq / p.Hkv;
-  Builder bd{P};
+  Builder bd;
+  bd.P = P;
   bd.L = make_layout(p);
   const Layout& L = bd.L;
   const Groups& g = L.g;
