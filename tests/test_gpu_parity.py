@@ -327,3 +327,18 @@ def test_random_configs(ctx, seed):
         [np.arange(S - 64, S), np.random.default_rng(seed).choice(S, 512, replace=False)]))
     rep = full_check(ctx, S, 4, 2, mod, heads, q, k, v, rows=rows)
     say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(1, 1), (16, 2), (6, 6)])
+def test_head_counts(ctx, Hq, Hkv):
+    """One head, a GQA ratio of 8, and one KV head per query head."""
+    say(f"[gpu] Hq={Hq} Hkv={Hkv}")
+    S = 3000
+    mod = _mm_layout(S, 9)
+    q, k, v = _rand_qkv(S, Hq, Hkv, seed=40 + Hq, scale_k=1.5)
+    kinds = [C.global_head(C.ashape(64, 300)), C.qboundary_head({0: C.ashape(32, 200), 1: C.vslash(30, 20)}),
+             C.global_head(C.grid(20, 40)),
+             C.boundary2d_head({0: C.ashape(32, 200), 1: C.grid(20, 40)}, {(0, 1): C.vert(40), (1, 0): C.dense()})]
+    heads = [kinds[h % 4] for h in range(Hq)]
+    rep = full_check(ctx, S, Hq, Hkv, mod, heads, q, k, v)
+    say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
