@@ -12,10 +12,11 @@
 // Vertical-Slash top-k (Appendix C.3): the n largest scores of [0, L),
 // ties to the smaller index, as an ascending index list. Radix select on the
 // fp32 bit patterns (scores are non-negative, so bits order like values):
-// four 8-bit digit passes with an LDS histogram find the n-th largest value
-// T; then one ordered pass keeps every score > T and the first
-// (n - #greater) indices equal to T. All counts are integers, so the result
-// does not depend on thread timing.
+// four 8-bit digit passes with per-wave LDS histograms find the n-th largest
+// value T; then one ordered pass (wave prefix sums, eight elements per
+// thread) keeps every score > T and the first (n - #greater) indices equal
+// to T. All counts are integers, so the result does not depend on thread
+// timing.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -84,13 +85,18 @@ __global__ void k_grid_pick(const GridJob* jobs, int njobs) {
 }
 
 constexpr int TK_THREADS = 1024;
+constexpr int TK_WAVES = TK_THREADS / 64;
+constexpr int TK_PER = 8;          // consecutive elements per thread in the selection pass
 
+// Radix select of the n-th largest fp32 bit pattern (scores are >= 0, so the
+// bit patterns order like the values), then an order-preserving selection:
+// every element above it, and the first `remaining` copies of it by index.
 __global__ __launch_bounds__(TK_THREADS) void k_topk(const TopkJob* jobs) {
   const TopkJob jb = jobs[blockIdx.x];
-  __shared__ int hist[256];
+  __shared__ int hist[TK_WAVES][256];
   __shared__ int sh_digit, sh_rem;
-  __shared__ int scan[TK_THREADS];
-  const int tid = threadIdx.x;
+  __shared__ int wgt[TK_WAVES], weq[TK_WAVES];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (jb.n <= 0) return;
   if (jb.n >= jb.L) {
     for (int i = tid; i < jb.L; i += TK_THREADS) jb.out[i] = i;
@@ -100,18 +106,24 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk(const TopkJob* jobs) {
   uint32_t prefix = 0, mask = 0;
   int remaining = jb.n;
   for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int b = tid; b < 256; b += TK_THREADS) hist[b] = 0;
+    for (int b = tid; b < TK_WAVES * 256; b += TK_THREADS) (&hist[0][0])[b] = 0;
     __syncthreads();
-    for (int i = tid; i < jb.L; i += TK_THREADS) {
+    for (int i = tid; i < jb.L; i += TK_THREADS) {      // one histogram per wave: fewer collisions
       const uint32_t x = bits[i];
-      if ((x & mask) == prefix) atomicAdd(&hist[(x >> shift) & 255], 1);
+      if ((x & mask) == prefix) atomicAdd(&hist[wave][(x >> shift) & 255], 1);
+    }
+    __syncthreads();
+    for (int b = tid; b < 256; b += TK_THREADS) {
+      int c = 0;
+      for (int w = 0; w < TK_WAVES; ++w) c += hist[w][b];
+      hist[0][b] = c;
     }
     __syncthreads();
     if (tid == 0) {
       int cum = 0, d = 255;
       for (; d > 0; --d) {
-        if (cum + hist[d] >= remaining) break;
-        cum += hist[d];
+        if (cum + hist[0][d] >= remaining) break;
+        cum += hist[0][d];
       }
       sh_digit = d;
       sh_rem = remaining - cum;
@@ -122,35 +134,50 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk(const TopkJob* jobs) {
     remaining = sh_rem;
     __syncthreads();
   }
-  // prefix = bit pattern of the n-th largest value; `remaining` of its copies are taken
+  // prefix = bit pattern T of the n-th largest value; `remaining` of its copies
+  // are taken. Output slot of a selected element i = (elements above T before
+  // i) + min(copies of T before i, remaining): ascending indices.
   const uint32_t T = prefix;
-  int out_base = 0, eq_base = 0;
-  for (int start = 0; start < jb.L; start += TK_THREADS) {
-    const int i = start + tid;
-    const uint32_t x = i < jb.L ? bits[i] : 0u;
-    const int gt = (i < jb.L && x > T) ? 1 : 0;
-    const int eq = (i < jb.L && x == T) ? 1 : 0;
-    // inclusive scan of eq (bits 0-15) and gt (bits 16-31) packed
-    scan[tid] = eq | (gt << 16);
-    __syncthreads();
-    for (int off = 1; off < TK_THREADS; off <<= 1) {
-      const int v = tid >= off ? scan[tid - off] : 0;
-      __syncthreads();
-      scan[tid] += v;
-      __syncthreads();
+  int gt_base = 0, eq_base = 0;          // counts before the current chunk
+  for (int start = 0; start < jb.L; start += TK_THREADS * TK_PER) {
+    const int i0 = start + tid * TK_PER;
+    uint32_t xs[TK_PER];
+    int cg = 0, ce = 0;
+#pragma unroll
+    for (int e = 0; e < TK_PER; ++e) {
+      xs[e] = i0 + e < jb.L ? bits[i0 + e] : 0u;
+      cg += (i0 + e < jb.L && xs[e] > T) ? 1 : 0;
+      ce += (i0 + e < jb.L && xs[e] == T) ? 1 : 0;
     }
-    const int inc = scan[tid];
-    const int eq_before = eq_base + (inc & 0xffff) - eq;
-    const int take_eq = eq && eq_before < remaining;
-    const int sel = gt | take_eq;
-    // selected before i in this chunk: greater ones + equal ones taken since the chunk start
-    const int gt_before = (inc >> 16) - gt;
-    const int pos = out_base + gt_before + min(eq_before, remaining) - min(eq_base, remaining);
-    if (sel && pos < jb.n) jb.out[pos] = i;
-    const int tot = scan[TK_THREADS - 1];
+    int sg = cg, se = ce;                // inclusive scan over the wave's lanes
+    for (int off = 1; off < 64; off <<= 1) {
+      const int a = __shfl_up(sg, off, 64), b2 = __shfl_up(se, off, 64);
+      if (lane >= off) { sg += a; se += b2; }
+    }
+    if (lane == 63) { wgt[wave] = sg; weq[wave] = se; }
     __syncthreads();
-    out_base += (tot >> 16) + max(0, min(eq_base + (tot & 0xffff), remaining) - min(eq_base, remaining));
-    eq_base += tot & 0xffff;
+    int pg = 0, pe = 0, tg = 0, te = 0;
+    for (int w = 0; w < TK_WAVES; ++w) {
+      if (w < wave) { pg += wgt[w]; pe += weq[w]; }
+      tg += wgt[w];
+      te += weq[w];
+    }
+    __syncthreads();                     // wgt/weq are rewritten by the next chunk
+    int g_before = gt_base + pg + sg - cg, e_before = eq_base + pe + se - ce;
+#pragma unroll
+    for (int e = 0; e < TK_PER; ++e) {
+      if (i0 + e < jb.L) {
+        const bool gt = xs[e] > T, eq = xs[e] == T;
+        if (gt || (eq && e_before < remaining)) {
+          const int pos = g_before + min(e_before, remaining);
+          if (pos < jb.n) jb.out[pos] = i0 + e;
+        }
+        g_before += gt ? 1 : 0;
+        e_before += eq ? 1 : 0;
+      }
+    }
+    gt_base += tg;
+    eq_base += te;
   }
 }
 
