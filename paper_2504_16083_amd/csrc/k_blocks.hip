@@ -252,24 +252,28 @@ __global__ __launch_bounds__(256) void k_blocks_count(const HeadDev* heads, cons
     rc[tid] = hd.kind == MMI_HEAD_2D ? li0 + tid : p;   // coordinate of the row for identity-order rules
   }
   __syncthreads();
-  if (tid == 0) {
-    int nv = 0, mp = -1, nr = 0;
-    for (int r = 0; r < B; ++r) {
-      if (rpos[r] < 0) break;
-      ++nv;
-      mp = max(mp, rpos[r]);
-      if (nr > 0 && rc[r] == rb[nr - 1] + 1) {
-        rb[nr - 1] = rc[r];
-      } else {
-        ra[nr] = rc[r];
-        rb[nr] = rc[r];
-        ++nr;
-      }
+  if (tid < B) {
+    // wave 0, one row per lane: the leading valid rows, their largest
+    // position and their runs of consecutive coordinates [ra, rb]
+    const int r = tid;
+    const uint64_t vm = __ballot(rpos[r] >= 0);
+    const int nv = ~vm ? __builtin_ctzll(~vm) : B;
+    const bool in = r < nv;
+    const bool start = in && (r == 0 || rc[r] != rc[r - 1] + 1);
+    const bool end = in && (r + 1 == nv || rc[r + 1] != rc[r] + 1);
+    const uint64_t sm = __ballot(start);
+    const uint64_t upto = r == B - 1 ? ~0ull : ((1ull << (r + 1)) - 1);
+    const int run = __popcll(sm & upto) - 1;          // the run row r belongs to
+    if (start) ra[run] = rc[r];
+    if (end) rb[run] = rc[r];
+    int mp = in ? rpos[r] : -1;
+    for (int off = 32; off > 0; off >>= 1) mp = max(mp, __shfl_xor(mp, off, 64));
+    if (r == 0) {
+      sh_nvalid = nv;
+      sh_maxpos = mp;
+      sh_nruns = __popcll(sm);
+      sh_count = 0;
     }
-    sh_nvalid = nv;
-    sh_maxpos = mp;
-    sh_nruns = nr;
-    sh_count = 0;
   }
   __syncthreads();
   const int maxpos = sh_maxpos, nruns = sh_nruns;
