@@ -17,12 +17,13 @@
 // the accumulator is already the P operand of the PV product.
 //
 // Pipeline: K/V blocks rotate through four LDS stages with one barrier per
-// block; the global loads of block t+3 are in flight while block t is
-// computed. Within a wave, the QK MFMAs of block t+1 are issued between the
-// softmax instructions of block t. Across waves, the first R waves run
-// [softmax(t) + QK(t+1)] then PV(t), while the other R waves run PV(t-1)
-// then [softmax(t) + QK(t+1)]: a SIMD holds one wave of each half, so one
-// wave's exponentials overlap the other wave's PV products.
+// block. Step t multiplies P(t)V(t), turns the scores of block t+1 into
+// P(t+1) and computes the scores of block t+2; the three share no data and
+// are issued interleaved within each wave (MFMA, then a share of the
+// softmax), because the vector ALU overlaps only MFMAs of the same wave.
+// Meanwhile block t+3 is written to its stage from registers, the global
+// loads of block t+4 are in flight and the key positions of block t+5 are
+// loading.
 // V stays row-major in LDS and is read into the PV operand with the gfx950
 // transpose read (ds_read_b64_tr_b16): in each 16-lane group, output lane i,
 // element e is element i%4 of the 8-byte row addressed by lane 4e + i/4.
