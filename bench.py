@@ -12,7 +12,10 @@ Also measured in the same run:
     flops = computed blocks x 4*64*64*128, divided by the kernel's duration
     from HIP events recorded on the stream it runs on;
   * cpu_baseline: the CPU oracle timed on a bounded sample of the same
-    workload on this host's cores, extrapolated to ms/layer.
+    workload on this host's cores, extrapolated to ms/layer;
+  * with --sdpa, as context only: PyTorch's flash scaled-dot-product
+    attention (dense causal, one call per KV group with GQA) on the same
+    tensors.
 """
 from __future__ import annotations
 
@@ -81,6 +84,8 @@ def parse():
     ap.add_argument("--dense-reps", type=int, default=1)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--sdpa", action="store_true",
+                    help="also time PyTorch's flash SDPA (dense causal) on the same inputs, as context")
     ap.add_argument("--cpu-rows", type=int, default=8)
     ap.add_argument("--pattern", default="method",
                     choices=["method", "ashape", "trishape", "sf_fixed", "sf_strided", "vslash", "grid", "qb_grid"],
@@ -136,6 +141,42 @@ def cpu_baseline(wl, q, k, v, rows_per_head, heads):
                        f"extrapolated as plan_time*Hq + row_time*S*Hq (measured {time.perf_counter() - t0:.1f} s, "
                        f"incl. {t_load:.1f} s bf16->fp64 load)"),
             "plan_s_per_head": plan_per_head, "row_ms": per_row * 1e3}
+
+
+def sdpa_context(wl, q, k, v, sparse_ms):
+    """PyTorch's flash SDPA, dense causal, on the same tensors: one call per
+    KV group (its G query heads against one K/V head, GQA), inputs copied to
+    [1, H, S, D] before timing. The math fallback is disabled (at these
+    lengths it would build the S x S matrix); if flash is unavailable the
+    result says so. Reported as context, not as a baseline of this method."""
+    import torch
+    import torch.nn.functional as F
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    G = wl.Hq // wl.Hkv
+    groups = []
+    for g in range(wl.Hkv):
+        groups.append((q[:, g * G:(g + 1) * G].permute(1, 0, 2).contiguous().unsqueeze(0),
+                       k[:, g].contiguous()[None, None], v[:, g].contiguous()[None, None]))
+    torch.cuda.synchronize()
+
+    def run():
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+            return [F.scaled_dot_product_attention(a, b, c, is_causal=True, enable_gqa=True)
+                    for a, b, c in groups]
+    try:
+        run()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run()
+        e1.record()
+        torch.cuda.synchronize()
+    except RuntimeError as err:
+        return {"backend": "torch flash SDPA", "error": str(err)[:200]}
+    t = e0.elapsed_time(e1)
+    useful = 4.0 * 128 * wl.Hq * wl.S * (wl.S + 1) / 2      # causal q.k pairs only
+    return {"backend": f"torch {torch.__version__} flash SDPA, per KV group", "ms": t,
+            "tflops_causal_pairs": useful / (t * 1e-3) / 1e12, "sparse_speedup": t / sparse_ms}
 
 
 def search_main(args):
@@ -299,6 +340,11 @@ def main():
                  "tflops": causal_blocks * FLOP_PER_BLOCK / (dms * 1e-3) / 1e12,
                  "speedup_sparse_vs_dense": dms / ms}
 
+    sdpa = None
+    if args.sdpa and args.workload == "mm":
+        sdpa = sdpa_context(wl, q, k, v, ms)
+        log(f"sdpa done: {sdpa}")
+
     cpu = None
     if not args.no_cpu:
         kinds, heads = set(), []
@@ -331,6 +377,7 @@ def main():
                      "traffic": attention_traffic(wl.name)},
         "dense": dense,
         "speedup_vs_dense": None if dense is None else dense["speedup_sparse_vs_dense"],
+        **({"sdpa_context": sdpa} if sdpa is not None else {}),
         "cpu_baseline": cpu,
         "wall_s": wall,
     }
