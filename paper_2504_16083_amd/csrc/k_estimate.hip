@@ -5,7 +5,7 @@
 // Pass 1 (k_est_lse): per query set and key chunk, running (max, sum) of
 //   2^(tau log2e q.k) per row -> partials; k_est_merge folds the chunks in
 //   a fixed order into log2-domain LSE.
-// Pass 2 (k_est_scores): per query set and 64-key tile of the key
+// Pass 2 (k_est_scores): per query set and run of 64-key tiles of the key
 //   coordinate system, A_hat tile through MFMA, then in LDS the column sums
 //   (v, written directly: each tile owns its keys) and the 127 diagonal
 //   partial sums of the tile; k_est_udiag adds the (at most two) tiles that
@@ -14,7 +14,8 @@
 // The query rows are contiguous positions [row0, row0+nrows), nrows <= 64,
 // and contiguous in the key coordinate system too (coordinate coord0 + r).
 // K rows are read straight from HBM into MFMA operands (each lane loads one
-// contiguous 128-byte half row); no LDS staging is needed for S^T = K Q^T.
+// contiguous 128-byte half row; the next tile's rows load while the current
+// one is reduced); no LDS staging is needed for S^T = K Q^T.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -32,14 +33,17 @@ __device__ __forceinline__ void load_q_operand(bf16x8 (&qr)[8], const Tensor& q,
   for (int s = 0; s < 8; ++s) qr[s] = pos >= 0 ? load16(row + 8 * s) : zero8();
 }
 
-// S^T tile of 32 keys x 32 queries; lane (c, h) holds keys 8i + 4h + j for query c.
-__device__ __forceinline__ f32x16 key_tile(const Tensor& k, int kvh, int kpos, int h,
-                                           const bf16x8 (&qr)[8]) {
+// This lane's half of key row kpos (zeros for kpos < 0): the K operand of
+// one 32-key S^T tile.
+__device__ __forceinline__ void load_key(bf16x8 (&ka)[8], const Tensor& k, int kvh, int kpos, int h) {
   const uint16_t* row = reinterpret_cast<const uint16_t*>(k.p) + (int64_t)kvh * k.sh +
                         (int64_t)max(kpos, 0) * k.ss + h * 64;
-  bf16x8 ka[8];
 #pragma unroll
   for (int s = 0; s < 8; ++s) ka[s] = kpos >= 0 ? load16(row + 8 * s) : zero8();
+}
+
+// S^T tile of 32 keys x 32 queries; lane (c, h) holds keys 8i + 4h + j for query c.
+__device__ __forceinline__ f32x16 key_product(const bf16x8 (&ka)[8], const bf16x8 (&qr)[8]) {
   f32x16 acc;
 #pragma unroll
   for (int x = 0; x < 16; ++x) acc[x] = 0.0f;
@@ -63,9 +67,12 @@ __global__ __launch_bounds__(128) void k_est_lse(const RowSet* sets, Tensor q, T
   const int k0 = ch * chunk_keys;
   const int k1 = min(k0 + chunk_keys, limit);
   float m = NEG_BIG, l = 0.0f;
+  bf16x8 ka[8];
+  load_key(ka, k, rs.kvh, k0 + c < k1 ? k0 + c : -1, h);
   for (int kb = k0; kb < k1; kb += 32) {
-    const int kp = kb + c < k1 ? kb + c : -1;
-    const f32x16 s = key_tile(k, rs.kvh, kp, h, qr);
+    const f32x16 s = key_product(ka, qr);
+    // the next tile's keys load while this one is reduced
+    if (kb + 32 < k1) load_key(ka, k, rs.kvh, kb + 32 + c < k1 ? kb + 32 + c : -1, h);
     float mx = NEG_BIG;
     float x[16];
 #pragma unroll
@@ -110,53 +117,81 @@ __global__ __launch_bounds__(64) void k_est_merge(const RowSet* sets) {
 }
 
 constexpr int APITCH = 65;
+constexpr int EST_TPW = 8;    // 64-key tiles per workgroup of the score pass
 
+// Each workgroup takes EST_TPW consecutive tiles of one job: the query rows
+// are loaded once, and the next tile's key positions and K rows load while
+// the current tile is reduced. The arithmetic of every tile is the same as
+// one tile per workgroup.
 __global__ __launch_bounds__(128) void k_est_scores(const EstJob* jobs, const RowSet* sets, Tensor q,
                                                     Tensor k) {
   __shared__ float ahat[B * APITCH];
+  __shared__ int kposl[B];      // key positions of the current tile, INT_BIG past L_c
   const EstJob jb = jobs[blockIdx.x];
-  const int t = blockIdx.y;
-  if (t >= jb.ntiles) return;
+  const int ta = blockIdx.y * EST_TPW;
+  if (ta >= jb.ntiles) return;
+  const int tb = min(ta + EST_TPW, jb.ntiles);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
   const int r = wave * 32 + c;
   const int qpos = r < jb.nrows ? jb.row0 + r : -1;
   const float lse2 = qpos >= 0 ? sets[jb.rowset].lse2[r] : 0.0f;
   bf16x8 qr[8];
   load_q_operand(qr, q, jb.head, qpos, h);
+  auto key_pos = [&](int kap) { return kap < jb.L_c ? (jb.keymap ? jb.keymap[kap] : kap) : -1; };
+  int kp[2];
+  bf16x8 ka[2][8];
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt) {
-    const int kap = t * B + kt * 32 + c;          // coordinate loaded by this lane
-    const int kp = kap < jb.L_c ? (jb.keymap ? jb.keymap[kap] : kap) : -1;
-    const f32x16 s = key_tile(k, jb.kvh, kp, h, qr);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int kk = kt * 32 + 8 * i + 4 * h + j;   // key index inside the tile
-        const int kap2 = t * B + kk;
-        const int kp2 = kap2 < jb.L_c ? (jb.keymap ? jb.keymap[kap2] : kap2) : INT_BIG;
-        const float a = (qpos >= 0 && kp2 <= qpos) ? fast_exp2(s[4 * i + j] * SC - lse2) : 0.0f;
-        ahat[kk * APITCH + r] = a;
-      }
+    kp[kt] = key_pos(ta * B + kt * 32 + c);
+    load_key(ka[kt], k, jb.kvh, kp[kt], h);
   }
-  __syncthreads();
-  {   // column sums: two threads per key, rows 0-31 and 32-63, then the pair
-    const int kk = tid >> 1, half = tid & 1;
-    float acc = 0.0f;
-    for (int rr = 32 * half; rr < 32 * half + 32; ++rr) acc += ahat[kk * APITCH + rr];
-    const float other = __shfl_xor(acc, 1);
-    const float tot = half == 0 ? acc + other : other + acc;
-    const int kap = t * B + kk;
-    if (half == 0 && kap < jb.L_c) jb.v[kap] = tot;
-  }
-  if (jb.dpart) {   // diagonal d = r - kk + 63, d in [0, 127)
-    const int d = tid;
-    float acc = 0.0f;
-    if (d < 127) {
-      const int rlo = max(0, d - 63), rhi = min(63, d);
-      for (int rr = rlo; rr <= rhi; ++rr) acc += ahat[(rr + 63 - d) * APITCH + rr];
+  for (int t = ta; t < tb; ++t) {
+    f32x16 s[2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) s[kt] = key_product(ka[kt], qr);
+    if (wave == 0 && h == 0) {
+      kposl[c] = kp[0] >= 0 ? kp[0] : INT_BIG;
+      kposl[32 + c] = kp[1] >= 0 ? kp[1] : INT_BIG;
     }
-    jb.dpart[(int64_t)t * 128 + d] = acc;
+    if (t + 1 < tb) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        kp[kt] = key_pos((t + 1) * B + kt * 32 + c);
+        load_key(ka[kt], k, jb.kvh, kp[kt], h);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int kk = kt * 32 + 8 * i + 4 * h + j;   // key index inside the tile
+          const int kp2 = kposl[kk];
+          const float a = (qpos >= 0 && kp2 <= qpos) ? fast_exp2(s[kt][4 * i + j] * SC - lse2) : 0.0f;
+          ahat[kk * APITCH + r] = a;
+        }
+    __syncthreads();
+    {   // column sums: two threads per key, rows 0-31 and 32-63, then the pair
+      const int kk = tid >> 1, half = tid & 1;
+      float acc = 0.0f;
+      for (int rr = 32 * half; rr < 32 * half + 32; ++rr) acc += ahat[kk * APITCH + rr];
+      const float other = __shfl_xor(acc, 1);
+      const float tot = half == 0 ? acc + other : other + acc;
+      const int kap = t * B + kk;
+      if (half == 0 && kap < jb.L_c) jb.v[kap] = tot;
+    }
+    if (jb.dpart) {   // diagonal d = r - kk + 63, d in [0, 127)
+      const int d = tid;
+      float acc = 0.0f;
+      if (d < 127) {
+        const int rlo = max(0, d - 63), rhi = min(63, d);
+        for (int rr = rlo; rr <= rhi; ++rr) acc += ahat[(rr + 63 - d) * APITCH + rr];
+      }
+      jb.dpart[(int64_t)t * 128 + d] = acc;
+    }
+    __syncthreads();    // ahat and kposl are rewritten by the next tile
   }
 }
 
@@ -193,7 +228,8 @@ hipError_t launch_est_lse(const RowSet* rs, int nrs, int max_chunks, Tensor q, T
 hipError_t launch_est_scores(const EstJob* jobs, int njobs, int max_tiles, const RowSet* rs, Tensor q,
                              Tensor k, hipStream_t st) {
   if (njobs <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_est_scores, dim3(njobs, max_tiles), dim3(128), 0, st, jobs, rs, q, k);
+  hipLaunchKernelGGL(k_est_scores, dim3(njobs, (max_tiles + EST_TPW - 1) / EST_TPW), dim3(128), 0, st, jobs, rs,
+                     q, k);
   return hipGetLastError();
 }
 
