@@ -75,7 +75,7 @@ struct OpDev {
   const int32_t* params;      // GRID: {sigma, phase}
   const int32_t* vsel; int32_t nv;
   const int32_t* ssel; int32_t ns;
-  int32_t* minsel;            // [nkblk] smallest selected key position per key block
+  int2* selpb;                // [nv] position and key block (from kbase) of each selected vertical
   const int32_t* keymap;      // coordinate -> position for VSLASH/VERT (nullptr = identity)
   int32_t kgrid;              // key group is Grid-ordered (VERT into a Grid group)
   const int32_t* kparams;     // that group's {sigma, phase}

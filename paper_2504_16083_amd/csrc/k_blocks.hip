@@ -6,7 +6,9 @@
 // same operation here.
 //
 // k_key_summaries: per key block the smallest key position (kminpos) and,
-//   per VS / VERT op, the smallest selected key position (minsel).
+//   per VS / VERT op, the position and key block of every selected vertical
+//   (selpb: a query block tests at most n_vertical selections instead of
+//   every key block).
 // k_blocks_count: one workgroup per (head, query block) sets the selected key
 //   blocks in an LDS bitmap with closed-form rules (ranges, per-block
 //   threshold tests, slash offsets), then stores the bitmap and its
@@ -40,21 +42,18 @@ __global__ __launch_bounds__(256) void k_kminpos(const HeadDev* heads) {
   if (hd.kmaxpos) hd.kmaxpos[j] = pad ? INT_BIG : mx;
 }
 
-__global__ __launch_bounds__(256) void k_minsel_init(OpDev* ops) {
-  const OpDev op = ops[blockIdx.x];
-  const int j = blockIdx.y * 256 + threadIdx.x;
-  if (op.minsel && j < op.nkblk) op.minsel[j] = INT_BIG;
-}
-
-__global__ __launch_bounds__(256) void k_minsel_scatter(OpDev* ops) {
+// Position and key block of every selected vertical: a query block selects
+// key block b for the verticals iff some selection in b has a position at or
+// below the block's largest query position.
+__global__ __launch_bounds__(256) void k_sel_blocks(OpDev* ops) {
   const OpDev op = ops[blockIdx.x];
   const int i = blockIdx.y * 256 + threadIdx.x;
-  if (!op.minsel || i >= op.nv) return;
+  if (!op.selpb || i >= op.nv) return;
   const int kap = op.vsel[i];
   const int pos = op.keymap ? op.keymap[kap] : kap;
   int local = kap;
   if (op.kgrid && op.kparams[0] > 0) local = grid_slot(grid_geo(op.L, op.kparams[0], op.kparams[1]), kap);
-  atomicMin(&op.minsel[local / B], pos);
+  op.selpb[i] = make_int2(pos, local / B);
 }
 
 hipError_t launch_key_summaries(const HeadDev* heads, int nheads, OpDev* ops, int nops, Groups g,
@@ -62,10 +61,8 @@ hipError_t launch_key_summaries(const HeadDev* heads, int nheads, OpDev* ops, in
   (void)g;
   if (nheads > 0 && max_nbk > 0)
     hipLaunchKernelGGL(k_kminpos, dim3(nheads, (max_nbk + 255) / 256), dim3(256), 0, st, heads);
-  if (nops > 0 && max_nbk > 0)
-    hipLaunchKernelGGL(k_minsel_init, dim3(nops, (max_nbk + 255) / 256), dim3(256), 0, st, ops);
   if (nops > 0 && max_sel > 0)
-    hipLaunchKernelGGL(k_minsel_scatter, dim3(nops, (max_sel + 255) / 256), dim3(256), 0, st, ops);
+    hipLaunchKernelGGL(k_sel_blocks, dim3(nops, (max_sel + 255) / 256), dim3(256), 0, st, ops);
   return hipGetLastError();
 }
 
@@ -109,6 +106,14 @@ __device__ __forceinline__ void set_threshold(uint32_t* bm, const int32_t* thr, 
   }
 }
 
+// key blocks kbase + b of the selected verticals whose position is <= lim
+__device__ __forceinline__ void set_verticals(uint32_t* bm, const OpDev& op, int kbase, int lim) {
+  for (int i = threadIdx.x; i < op.nv; i += blockDim.x) {
+    const int2 sb = op.selpb[i];
+    if (sb.x <= lim) set_bit(bm, kbase + sb.y);
+  }
+}
+
 // dense / A-shape / VS / static baselines over coordinates whose keys sit at
 // key block kbase + c / 64 (row coordinates as runs [ra, rb])
 __device__ void identity_rules(uint32_t* bm, const OpDev& op, const int* ra, const int* rb, int nruns,
@@ -140,7 +145,7 @@ __device__ void identity_rules(uint32_t* bm, const OpDev& op, const int* ra, con
       }
     }
   } else if (op.kind == MMI_OP_VSLASH) {
-    set_threshold(bm, op.minsel, kbase, op.nkblk, maxpos, false);
+    set_verticals(bm, op, kbase, maxpos);
     for (int idx = threadIdx.x; idx < op.ns; idx += blockDim.x) {
       const int o = op.ssel[idx];
       for (int r = 0; r < nruns; ++r) {
@@ -310,7 +315,7 @@ __global__ __launch_bounds__(256) void k_blocks_count(const HeadDev* heads, cons
       } else if (op.kind == MMI_OP_DENSE) {
         set_threshold(bm, hd.kminpos + kbase, kbase, nk, maxpos, false);
       } else if (op.kind == MMI_OP_VERT) {
-        set_threshold(bm, op.minsel, kbase, nk, maxpos, false);
+        set_verticals(bm, op, kbase, maxpos);
       }
     }
     if (tid == 0) set_bit(bm, qb);

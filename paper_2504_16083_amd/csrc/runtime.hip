@@ -568,7 +568,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
           e.nv = std::min(c.global.n_vertical, e.L_c);
           e.ns = std::min(c.global.n_slash, e.L_c);
           d.vsel = e.vsel; d.nv = e.nv; d.ssel = e.ssel; d.ns = e.ns;
-          d.minsel = dalloc<int32_t>(P, nb_all);
+          d.selpb = dalloc<int2>(P, d.nv);
         }
       }
       if (c.global.kind == MMI_OP_GRID) {
@@ -614,7 +614,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
           e.nv = std::min(o.n_vertical, e.L_c);
           e.ns = std::min(o.n_slash, e.L_c);
           d.vsel = e.vsel; d.nv = e.nv; d.ssel = e.ssel; d.ns = e.ns;
-          d.minsel = dalloc<int32_t>(P, nb_all);
+          d.selpb = dalloc<int2>(P, d.nv);
         }
         P->ops.push_back(d);
         H.est.push_back(e);
@@ -652,7 +652,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
             e.nv = std::min(o.n_vertical, e.L_c);
             e.ns = std::min(o.n_slash, e.L_c);
             d.vsel = e.vsel; d.nv = e.nv; d.ssel = e.ssel; d.ns = e.ns;
-            d.minsel = dalloc<int32_t>(P, d.nkblk);
+            d.selpb = dalloc<int2>(P, d.nv);
           }
         }
         P->ops[n0 + gi * g.n + gi] = d;
@@ -681,7 +681,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
               e.nv = std::min(o.n_vertical, e.L_c);
             }
             d.vsel = e.vsel; d.nv = e.nv;
-            d.minsel = dalloc<int32_t>(P, d.nkblk);
+            d.selpb = dalloc<int2>(P, d.nv);
           }
           P->ops[n0 + a * g.n + b2] = d;
           H.est[a * g.n + b2] = e;
