@@ -31,10 +31,20 @@ __global__ __launch_bounds__(256) void k_grid_fold(const GridJob* jobs) {
   __shared__ int bp[256];
   float best = -1.0f;
   int bestp = 0x7fffffff;
+  constexpr int U = 16;   // loads in flight per thread; the sum keeps ascending t order
   for (int p = threadIdx.x; p < s; p += 256) {
     float acc = 0.0f;
     int n = 0;
-    for (int x = p; x < jb.L_c; x += s) {
+    int x = p;
+    for (; x + (U - 1) * s < jb.L_c; x += U * s) {
+      float t[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) t[u] = jb.v[x + u * s];
+#pragma unroll
+      for (int u = 0; u < U; ++u) acc += t[u];
+      n += U;
+    }
+    for (; x < jb.L_c; x += s) {
       acc += jb.v[x];
       ++n;
     }
