@@ -118,9 +118,16 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk(const TopkJob* jobs) {
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int b = tid; b < TK_WAVES * 256; b += TK_THREADS) (&hist[0][0])[b] = 0;
     __syncthreads();
-    for (int i = tid; i < jb.L; i += TK_THREADS) {      // one histogram per wave: fewer collisions
-      const uint32_t x = bits[i];
-      if ((x & mask) == prefix) atomicAdd(&hist[wave][(x >> shift) & 255], 1);
+    // one histogram per wave (fewer collisions); eight loads in flight per
+    // thread (the counts do not depend on the order they are added in)
+    constexpr int HU = 8;
+    for (int i0 = tid; i0 < jb.L; i0 += TK_THREADS * HU) {
+      uint32_t xs[HU];
+#pragma unroll
+      for (int u = 0; u < HU; ++u) xs[u] = i0 + u * TK_THREADS < jb.L ? bits[i0 + u * TK_THREADS] : 0u;
+#pragma unroll
+      for (int u = 0; u < HU; ++u)
+        if (i0 + u * TK_THREADS < jb.L && (xs[u] & mask) == prefix) atomicAdd(&hist[wave][(xs[u] >> shift) & 255], 1);
     }
     __syncthreads();
     for (int b = tid; b < 256; b += TK_THREADS) {
@@ -149,16 +156,22 @@ __global__ __launch_bounds__(TK_THREADS) void k_topk(const TopkJob* jobs) {
   // i) + min(copies of T before i, remaining): ascending indices.
   const uint32_t T = prefix;
   int gt_base = 0, eq_base = 0;          // counts before the current chunk
+  uint32_t nx[TK_PER];                   // the next chunk, loading while this one is scanned
+#pragma unroll
+  for (int e = 0; e < TK_PER; ++e) nx[e] = tid * TK_PER + e < jb.L ? bits[tid * TK_PER + e] : 0u;
   for (int start = 0; start < jb.L; start += TK_THREADS * TK_PER) {
     const int i0 = start + tid * TK_PER;
     uint32_t xs[TK_PER];
     int cg = 0, ce = 0;
 #pragma unroll
     for (int e = 0; e < TK_PER; ++e) {
-      xs[e] = i0 + e < jb.L ? bits[i0 + e] : 0u;
+      xs[e] = nx[e];
       cg += (i0 + e < jb.L && xs[e] > T) ? 1 : 0;
       ce += (i0 + e < jb.L && xs[e] == T) ? 1 : 0;
     }
+    const int n0 = i0 + TK_THREADS * TK_PER;
+#pragma unroll
+    for (int e = 0; e < TK_PER; ++e) nx[e] = n0 + e < jb.L ? bits[n0 + e] : 0u;
     int sg = cg, se = ce;                // inclusive scan over the wave's lanes
     for (int off = 1; off < 64; off <<= 1) {
       const int a = __shfl_up(sg, off, 64), b2 = __shfl_up(se, off, 64);
