@@ -154,15 +154,35 @@ def _head_cfg(h) -> mmi_head_cfg:
     return c
 
 
+def _cfg_key(h):
+    """Value of a head config (its ops are immutable; the config itself may
+    be changed between calls, so it is keyed by what it holds)."""
+    return (h.kind, h.op, tuple(sorted(h.intra.items())), tuple(sorted(h.cross.items())))
+
+
+_cfg_cache = {}      # value of one head config -> marshalled mmi_head_cfg
+_cfgs_cache = {}     # values of a head list -> marshalled array
+_CACHE_MAX = 256
+
+
 def head_cfgs(heads) -> ct.Array:
-    """mmi_head_cfg array for the heads (a config object repeated over heads
-    is marshalled once)."""
-    arr = (mmi_head_cfg * len(heads))()
-    done = {}
-    for i, h in enumerate(heads):
-        if id(h) not in done:
-            done[id(h)] = _head_cfg(h)
-        arr[i] = done[id(h)]
+    """mmi_head_cfg array for the heads. Marshalled configs are cached by
+    value (the library reads the array only during the call it is passed to,
+    so one array may serve several plans)."""
+    keys = tuple(_cfg_key(h) for h in heads)
+    arr = _cfgs_cache.get(keys)
+    if arr is None:
+        arr = (mmi_head_cfg * len(heads))()
+        for i, (h, key) in enumerate(zip(heads, keys)):
+            c = _cfg_cache.get(key)
+            if c is None:
+                if len(_cfg_cache) >= _CACHE_MAX:
+                    _cfg_cache.clear()
+                c = _cfg_cache[key] = _head_cfg(h)
+            arr[i] = c
+        if len(_cfgs_cache) >= _CACHE_MAX:
+            _cfgs_cache.clear()
+        _cfgs_cache[keys] = arr
     return arr
 
 

@@ -125,3 +125,18 @@ def test_head_cfg_marshalling_fills_every_op():
     for cid in (2, 4):
         heads = workloads.by_id(cid).heads
         assert bytes(mmi.head_cfgs(heads)) == bytes(full(heads))
+
+
+def test_head_cfg_cache_follows_values():
+    """Marshalled configs are cached by value: a config changed in place
+    marshals to its new value, equal configs to equal bytes."""
+    h = C.global_head(C.ashape(128, 1024))
+    a = bytes(mmi.head_cfgs([h, h]))
+    h.op = C.ashape(128, 2048)
+    b = bytes(mmi.head_cfgs([h, h]))
+    assert a != b
+    assert b == bytes(mmi.head_cfgs([C.global_head(C.ashape(128, 2048))] * 2))
+    q = C.qboundary_head({1: C.grid(4, 8)})
+    before = bytes(mmi.head_cfgs([q]))
+    q.intra[0] = C.ashape(64, 512)
+    assert bytes(mmi.head_cfgs([q])) != before
