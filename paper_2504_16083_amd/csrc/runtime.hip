@@ -13,6 +13,7 @@
 #include <mutex>
 #include <stdexcept>
 #include <string>
+#include <functional>
 #include <vector>
 
 #include "device.hpp"
@@ -179,17 +180,29 @@ static T* dalloc(mmi_plan* P, size_t count) {
   return reinterpret_cast<T*>(p);
 }
 
-// The host copy is kept in the plan until it is destroyed, so the
-// asynchronous copy never reads freed memory.
-template <typename T>
-static T* upload(mmi_plan* P, const std::vector<T>& v) {
-  T* d = dalloc<T>(P, v.size());
-  if (!v.empty()) {
-    P->keep.emplace_back(reinterpret_cast<const uint8_t*>(v.data()),
-                         reinterpret_cast<const uint8_t*>(v.data()) + v.size() * sizeof(T));
-    HIPCHK(hipMemcpyAsync(d, P->keep.back().data(), v.size() * sizeof(T), hipMemcpyHostToDevice, P->stream));
+// Several host arrays sent as one device allocation and one copy (fewer
+// small host-to-device copies per plan); each array's device address is
+// handed to its setter when the pack is sent. The host copy is kept in the
+// plan until it is destroyed, so the asynchronous copy never reads freed
+// memory.
+struct Pack {
+  std::vector<uint8_t> host;
+  std::vector<std::function<void(uint8_t*)>> set;
+  template <typename T>
+  void add(const std::vector<T>& v, T*& out) {
+    const size_t off = (host.size() + 255) & ~(size_t)255;
+    host.resize(off + std::max<size_t>(v.size(), 1) * sizeof(T));
+    if (!v.empty()) std::memcpy(host.data() + off, v.data(), v.size() * sizeof(T));
+    T** slot = &out;
+    set.emplace_back([slot, off](uint8_t* d) { *slot = reinterpret_cast<T*>(d + off); });
   }
-  return d;
+};
+
+static void send(mmi_plan* P, Pack& pk) {
+  uint8_t* d = dalloc<uint8_t>(P, pk.host.size());
+  P->keep.push_back(std::move(pk.host));
+  HIPCHK(hipMemcpyAsync(d, P->keep.back().data(), P->keep.back().size(), hipMemcpyHostToDevice, P->stream));
+  for (auto& f : pk.set) f(d);
 }
 
 static void free_plan_buffers(mmi_plan* P) {
@@ -498,8 +511,14 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   // positions of each modality
   std::vector<int32_t> toff_by_mod(MMI_MAX_MODALITIES, 0);
   for (int gi = 0; gi < g.n; ++gi) toff_by_mod[g.mod[gi]] = g.toff[gi];
-  Segment* d_segs = upload(P, L.segs);
-  int32_t* d_toff = upload(P, toff_by_mod);
+  Segment* d_segs = nullptr;
+  int32_t* d_toff = nullptr;
+  {
+    Pack pk;
+    pk.add(L.segs, d_segs);
+    pk.add(toff_by_mod, d_toff);
+    send(P, pk);
+  }
   bd.d_tpos = P->d_tpos = dalloc<int32_t>(P, S);
   bool qb_grid = false;
   for (int h = 0; h < p.Hq; ++h) qb_grid |= cfgs[h].kind == MMI_HEAD_QBOUNDARY && qb_grid_mods(g, cfgs[h]) > 0;
@@ -720,24 +739,33 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   // estimation -> choices
   const Tensor tq{q, p.q_stride_s, p.q_stride_h}, tk{k, p.k_stride_s, p.k_stride_h};
   for (auto& e : P->ev) HIPCHK(hipEventCreate(&e));
-  RowSet* d_rs = upload(P, bd.rowsets);
-  EstJob* d_jobs = upload(P, bd.jobs);
+  RowSet* d_rs = nullptr;
+  EstJob* d_jobs = nullptr;
+  GridJob* d_g = nullptr;
+  TopkJob* d_t = nullptr;
+  QbOrderJob* d_qj = nullptr;
+  {
+    Pack pk;
+    pk.add(bd.rowsets, d_rs);
+    pk.add(bd.jobs, d_jobs);
+    pk.add(bd.gjobs, d_g);
+    pk.add(bd.tjobs, d_t);
+    pk.add(P->heads, P->d_heads);
+    pk.add(P->ops, P->d_ops);
+    pk.add(qjobs, d_qj);
+    send(P, pk);
+  }
   HIPCHK(hipEventRecord(P->ev[0], st));
   HIPCHK(launch_est_lse(d_rs, (int)bd.rowsets.size(), bd.max_chunks, tq, tk, bd.chunk_keys, st));
   HIPCHK(launch_est_scores(d_jobs, (int)bd.jobs.size(), bd.max_tiles, d_rs, tq, tk, st));
   HIPCHK(launch_est_udiag(d_jobs, (int)bd.jobs.size(), bd.max_L, st));
   HIPCHK(hipEventRecord(P->ev[1], st));
-  GridJob* d_g = upload(P, bd.gjobs);
   HIPCHK(launch_grid_search(d_g, (int)bd.gjobs.size(), bd.max_cands, st));
-  TopkJob* d_t = upload(P, bd.tjobs);
   HIPCHK(launch_topk(d_t, (int)bd.tjobs.size(), st));
   HIPCHK(hipEventRecord(P->ev[2], st));
 
   // permutations, key summaries, block counts
-  P->d_heads = upload(P, P->heads);
-  P->d_ops = upload(P, P->ops);
   HIPCHK(launch_perms(P->d_heads, p.Hq, P->d_ops, g, bd.d_tpos, S, max_slots, st));
-  QbOrderJob* d_qj = upload(P, qjobs);
   HIPCHK(launch_qb_order(d_qj, (int)qjobs.size(), d_modpos, S, st));
   HIPCHK(launch_key_summaries(P->d_heads, p.Hq, P->d_ops, (int)P->ops.size(), g, max_nbk, bd.max_sel, st));
   const int chunk = ctx->chunk_blocks;
@@ -797,9 +825,14 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   P->d_splits = dalloc<SplitRow>(P, P->nsplit);
   P->d_part_o = dalloc<float>(P, (size_t)std::max<int64_t>(P->nparts, 1) * B * R * D);
   P->d_part_ml = dalloc<float>(P, (size_t)std::max<int64_t>(P->nparts, 1) * B * R * 2);
-  int64_t* d_ib = upload(P, item_base);
-  int64_t* d_pb = upload(P, part_base);
-  int64_t* d_sb = upload(P, split_base);
+  int64_t *d_ib = nullptr, *d_pb = nullptr, *d_sb = nullptr;
+  {
+    Pack pk;
+    pk.add(item_base, d_ib);
+    pk.add(part_base, d_pb);
+    pk.add(split_base, d_sb);
+    send(P, pk);
+  }
   HIPCHK(launch_work_fill(P->d_heads, p.Hq, d_ib, d_pb, d_sb, max_groups, P->d_items, P->d_splits, st));
   HIPCHK(hipEventRecord(P->ev[3], st));
   P->nnz_all = nnz_all;
