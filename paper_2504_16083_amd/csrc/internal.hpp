@@ -104,7 +104,7 @@ struct HeadDev {
   // (g / rho) * R * rho + g % rho + r * rho; rho is chosen per head.
   int32_t gcap;               // capacity of the per-group arrays (>= groups for any stride)
   int32_t rho_alt[2];         // extra row-stride candidates besides 1, 2, 4, 8 (0 = none)
-  int32_t* gp;                // [2] chosen row stride rho of the groups, number of groups
+  int32_t* gp;                // [3] chosen row stride rho, number of groups, index of rho among the candidates
   int32_t* gcount;            // [groups] union sizes
   int32_t* growptr;           // [ngroups+1]
   int32_t* gcol;              // [gnnz] union entries: key block, select flags << 16, mask flags << 24
@@ -170,9 +170,10 @@ hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* op
 // rho_alt (smallest total union, ties to the earlier candidate); cand: int64
 // scratch [nheads][NRHO].
 constexpr int NRHO = 6;
-hipError_t launch_group_stride(const HeadDev* heads, int nheads, int R, int max_groups, int64_t* cand,
+hipError_t launch_group_stride(const HeadDev* heads, int nheads, int R, int max_groups, int64_t* cand, int32_t* gcnt,
                                hipStream_t st);
-hipError_t launch_group_count(const HeadDev* heads, int nheads, int R, int max_groups, hipStream_t st);
+hipError_t launch_group_count(const HeadDev* heads, int nheads, const int32_t* gcnt, int max_groups,
+                              hipStream_t st);
 // totals[head] = {nnz, gnnz, nitems, nsplit, nparts}
 constexpr int NTOT = 5;
 // Work-item length per head: max(min_chunk, ceil(gnnz_head / items_per_head)).

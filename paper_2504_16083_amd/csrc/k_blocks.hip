@@ -364,7 +364,10 @@ __device__ __forceinline__ int rho_candidate(const HeadDev& hd, int c) {
   return c < 4 ? 1 << c : hd.rho_alt[c - 4];
 }
 
-__global__ __launch_bounds__(256) void k_group_eval(const HeadDev* heads, int R, int64_t* cand) {
+// Union size of every group for every candidate stride (gcnt[head][c][g]),
+// and their per-head totals (cand).
+__global__ __launch_bounds__(256) void k_group_eval(const HeadDev* heads, int R, int64_t* cand, int32_t* gcnt,
+                                                    int max_groups) {
   const HeadDev hd = heads[blockIdx.x];
   const int g = blockIdx.y;
   __shared__ int sh;
@@ -376,8 +379,10 @@ __global__ __launch_bounds__(256) void k_group_eval(const HeadDev* heads, int R,
     __syncthreads();
     atomicAdd(&sh, union_count(hd, g, R, rho));
     __syncthreads();
-    if (threadIdx.x == 0) atomicAdd(reinterpret_cast<unsigned long long*>(&cand[blockIdx.x * NRHO + c]),
-                                    (unsigned long long)sh);
+    if (threadIdx.x == 0) {
+      atomicAdd(reinterpret_cast<unsigned long long*>(&cand[blockIdx.x * NRHO + c]), (unsigned long long)sh);
+      gcnt[((int64_t)blockIdx.x * NRHO + c) * max_groups + g] = sh;
+    }
     __syncthreads();
   }
 }
@@ -391,32 +396,31 @@ __global__ void k_group_pick(const HeadDev* heads, int nheads, int R, const int6
     if (rho_candidate(hd, c) > 0 && cand[h * NRHO + c] < cand[h * NRHO + best]) best = c;
   hd.gp[0] = rho_candidate(hd, best);
   hd.gp[1] = groups_for(hd.nbq, R, hd.gp[0]);
+  hd.gp[2] = best;
 }
 
 hipError_t launch_group_stride(const HeadDev* heads, int nheads, int R, int max_groups, int64_t* cand,
-                               hipStream_t st) {
+                               int32_t* gcnt, hipStream_t st) {
   if (nheads <= 0 || max_groups <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_zero64, dim3((nheads * NRHO + 255) / 256), dim3(256), 0, st, cand, nheads * NRHO);
-  hipLaunchKernelGGL(k_group_eval, dim3(nheads, max_groups), dim3(256), 0, st, heads, R, cand);
+  hipLaunchKernelGGL(k_group_eval, dim3(nheads, max_groups), dim3(256), 0, st, heads, R, cand, gcnt, max_groups);
   hipLaunchKernelGGL(k_group_pick, dim3((nheads + 63) / 64), dim3(64), 0, st, heads, nheads, R, cand);
   return hipGetLastError();
 }
 
-__global__ __launch_bounds__(256) void k_group_count(const HeadDev* heads, int R) {
+// The chosen stride's union sizes (counted by k_group_eval).
+__global__ __launch_bounds__(256) void k_group_count(const HeadDev* heads, const int32_t* gcnt, int max_groups) {
   const HeadDev hd = heads[blockIdx.x];
-  const int gr = blockIdx.y;
+  const int gr = blockIdx.y * 256 + threadIdx.x;
   if (gr >= hd.gp[1]) return;
-  __shared__ int sh_count;
-  if (threadIdx.x == 0) sh_count = 0;
-  __syncthreads();
-  atomicAdd(&sh_count, union_count(hd, gr, R, hd.gp[0]));
-  __syncthreads();
-  if (threadIdx.x == 0) hd.gcount[gr] = sh_count;
+  hd.gcount[gr] = gcnt[((int64_t)blockIdx.x * NRHO + hd.gp[2]) * max_groups + gr];
 }
 
-hipError_t launch_group_count(const HeadDev* heads, int nheads, int R, int max_groups, hipStream_t st) {
+hipError_t launch_group_count(const HeadDev* heads, int nheads, const int32_t* gcnt, int max_groups,
+                              hipStream_t st) {
   if (nheads <= 0 || max_groups <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_group_count, dim3(nheads, max_groups), dim3(256), 0, st, heads, R);
+  hipLaunchKernelGGL(k_group_count, dim3(nheads, (max_groups + 255) / 256), dim3(256), 0, st, heads, gcnt,
+                     max_groups);
   return hipGetLastError();
 }
 

@@ -721,7 +721,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
     }
     const int max_rho = std::max(8, std::max(hd.rho_alt[0], hd.rho_alt[1]));
     hd.gcap = (hd.nbq + R - 1) / R + max_rho;   // >= groups_for(nbq, R, rho) for every candidate
-    hd.gp = dalloc<int32_t>(P, 2);
+    hd.gp = dalloc<int32_t>(P, 3);
     hd.gcount = dalloc<int32_t>(P, hd.gcap);
     hd.growptr = dalloc<int32_t>(P, hd.gcap + 1);
     hd.chunklen = dalloc<int32_t>(P, 1);
@@ -771,8 +771,9 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   const int chunk = ctx->chunk_blocks;
   HIPCHK(launch_blocks_count(P->d_heads, p.Hq, P->d_ops, g, max_nbq, st));
   int64_t* d_cand = dalloc<int64_t>(P, (size_t)p.Hq * NRHO);
-  HIPCHK(launch_group_stride(P->d_heads, p.Hq, R, max_groups, d_cand, st));
-  HIPCHK(launch_group_count(P->d_heads, p.Hq, R, max_groups, st));
+  int32_t* d_gcnt = dalloc<int32_t>(P, (size_t)p.Hq * NRHO * std::max(max_groups, 1));
+  HIPCHK(launch_group_stride(P->d_heads, p.Hq, R, max_groups, d_cand, d_gcnt, st));
+  HIPCHK(launch_group_count(P->d_heads, p.Hq, d_gcnt, max_groups, st));
   const size_t ntot = (size_t)p.Hq * NTOT;
   int64_t* d_tot = dalloc<int64_t>(P, ntot);
   const int items_per_head = std::max(1, ctx->items_per_layer / p.Hq);
