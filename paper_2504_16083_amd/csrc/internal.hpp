@@ -176,8 +176,9 @@ hipError_t launch_group_count(const HeadDev* heads, int nheads, const int32_t* g
                               hipStream_t st);
 // totals[head] = {nnz, gnnz, nitems, nsplit, nparts}
 constexpr int NTOT = 5;
-// Work-item length per head: max(min_chunk, ceil(gnnz_head / items_per_head)).
-hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int min_chunk, int items_per_head,
+// Work-item length per head: max(min_chunk, ceil(gnnz_head / items_per_head),
+// avg_factor x the head's average group union) (avg_factor 0: no such floor).
+hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int min_chunk, int items_per_head, int avg_factor,
                               int64_t* totals, hipStream_t st);
 hipError_t launch_blocks_fill(const HeadDev* heads, int nheads, int max_nbq, int R, int max_groups,
                               hipStream_t st);

@@ -445,7 +445,7 @@ __device__ int block_exscan(int v, int* buf, int& excl) {
 }
 
 __global__ __launch_bounds__(SCAN_T) void k_blocks_scan(const HeadDev* heads, int min_chunk, int items_per_head,
-                                                        int64_t* totals) {
+                                                        int avg_factor, int64_t* totals) {
   const HeadDev hd = heads[blockIdx.x];
   __shared__ int buf[SCAN_T];
   int c_nnz = 0;
@@ -469,7 +469,9 @@ __global__ __launch_bounds__(SCAN_T) void k_blocks_scan(const HeadDev* heads, in
   }
   // long unions are split so that no work item holds much more than a
   // 1/items_per_head share of the head's work
-  const int chunk = max(min_chunk, (int)(((int64_t)c_g + items_per_head - 1) / items_per_head));
+  int chunk = max(min_chunk, (int)(((int64_t)c_g + items_per_head - 1) / items_per_head));
+  if (avg_factor > 0 && ngroups > 0)
+    chunk = max(chunk, (int)min<int64_t>(INT_BIG, (int64_t)avg_factor * (((int64_t)c_g + ngroups - 1) / ngroups)));
   int c_items = 0, c_split = 0, c_parts = 0;
   for (int start = 0; start < ngroups; start += SCAN_T) {
     const int i = start + threadIdx.x;
@@ -498,9 +500,10 @@ __global__ __launch_bounds__(SCAN_T) void k_blocks_scan(const HeadDev* heads, in
 }
 
 hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int min_chunk, int items_per_head,
-                              int64_t* totals, hipStream_t st) {
+                              int avg_factor, int64_t* totals, hipStream_t st) {
   if (nheads <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_blocks_scan, dim3(nheads), dim3(SCAN_T), 0, st, heads, min_chunk, items_per_head, totals);
+  hipLaunchKernelGGL(k_blocks_scan, dim3(nheads), dim3(SCAN_T), 0, st, heads, min_chunk, items_per_head, avg_factor,
+                     totals);
   return hipGetLastError();
 }
 

@@ -777,7 +777,14 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   const size_t ntot = (size_t)p.Hq * NTOT;
   int64_t* d_tot = dalloc<int64_t>(P, ntot);
   const int items_per_head = std::max(1, ctx->items_per_layer / p.Hq);
-  HIPCHK(launch_blocks_scan(P->d_heads, p.Hq, chunk, items_per_head, d_tot, st));
+  // When the row groups alone already give the target number of work items,
+  // only groups far above their head's average are split (a split puts
+  // chunks of one union side by side on an XCD, which share no key blocks,
+  // in place of neighbouring groups, which do).
+  int64_t groups_all = 0;
+  for (const auto& hd : P->heads) groups_all += (hd.nbq + R - 1) / R;
+  const int split_above_avg = groups_all >= ctx->items_per_layer ? 6 : 0;
+  HIPCHK(launch_blocks_scan(P->d_heads, p.Hq, chunk, items_per_head, split_above_avg, d_tot, st));
   if (ctx->pinned_n < ntot) {
     if (ctx->pinned) HIPCHK(hipHostFree(ctx->pinned));
     ctx->pinned = nullptr;
