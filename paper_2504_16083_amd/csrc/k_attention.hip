@@ -166,7 +166,7 @@ struct EntryStream {
 // turn. Runs of XCD_RUN consecutive items go to one XCD, and the runs are
 // interleaved across XCDs, so neighbouring row groups (which share key
 // blocks) meet in one L2 while heavy and light heads stay spread out.
-constexpr int XCD_RUN = 16;
+constexpr int XCD_RUN = 32;
 
 __device__ __forceinline__ int64_t item_of_block(int64_t b) {
   const int64_t xcd = b & 7, k = b >> 3;
