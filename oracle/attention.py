@@ -31,7 +31,11 @@ def attend(qvec, K, V, keys, scale):
 def head_rows(hp: P.HeadPlan, Qh, K, V, rows, scale=None):
     """O [len(rows), D] and LSE [len(rows)] for the given query positions.
 
-    Qh: fp64 [S, D] or a callable positions -> rows; K, V: fp64 [S, D]."""
+    Qh: fp64 [S, D] or a callable positions -> rows; K, V: fp64 [S, D].
+    Rows of one permuted query block share that block's selected key
+    blocks, so their logits come from one product with the union of those
+    keys; each row then keeps only its own causal keys (k <= q) and takes
+    the plain softmax over them."""
     scale = estimate.tau(K.shape[1]) if scale is None else scale
     rows = np.asarray(rows, dtype=np.int64)
     qv = Qh(rows) if callable(Qh) else Qh[rows]
@@ -40,11 +44,26 @@ def head_rows(hp: P.HeadPlan, Qh, K, V, rows, scale=None):
     slot_of = np.full(hp.S, -1, dtype=np.int64)
     valid = hp.qperm >= 0
     slot_of[hp.qperm[valid]] = np.nonzero(valid)[0]
-    for n, q in enumerate(rows):
-        i = int(slot_of[q]) // P.B
+    qblk = slot_of[rows] // P.B
+    blocks = np.unique(qblk)
+    # gathered key rows go to buffers allocated once (sized for the largest
+    # key set) and reused by every block
+    nmax = max((len(hp.blocks[i]) for i in blocks), default=0) * P.B
+    kbuf, vbuf = np.empty((nmax, K.shape[1])), np.empty((nmax, V.shape[1]))
+    for i in blocks:
+        sel = np.nonzero(qblk == i)[0]
         ks = np.concatenate([hp.kperm[j * P.B:(j + 1) * P.B] for j in hp.blocks[i]])
-        keys = np.sort(ks[(ks >= 0) & ((ks <= q) | (not hp.causal))])
-        O[n], L[n] = attend(qv[n], K, V, keys, scale)
+        keys = np.sort(ks[ks >= 0])
+        Kk = np.take(K, keys, axis=0, out=kbuf[:len(keys)], mode="clip")   # keys are in range
+        Vk = np.take(V, keys, axis=0, out=vbuf[:len(keys)], mode="clip")
+        s = scale * (qv[sel] @ Kk.T)                            # [rows of block i, keys]
+        if hp.causal:
+            s = np.where(keys[None, :] <= rows[sel][:, None], s, -np.inf)
+        m = s.max(axis=1)
+        e = np.exp(s - m[:, None])                              # masked keys give exactly 0
+        l = e.sum(axis=1)
+        O[sel] = (e / l[:, None]) @ Vk
+        L[sel] = m + np.log(l)
     return O, L
 
 

@@ -12,7 +12,7 @@ Reductions of A_hat used by the patterns, in a key coordinate system kappa
 where kappa_r is row r's own coordinate. L_c = 1 + the largest coordinate
 whose key is visible from some row of R.
 
-Pinned in tests/test_oracle_estimate.py: LSE against scipy's logsumexp,
+Pinned in tests/test_oracle_core.py: LSE against scipy's logsumexp,
 each A_hat row sums to 1, v sums to |R|, u against a brute-force double loop.
 """
 import math

@@ -36,26 +36,39 @@ def candidates(lo: int, hi: int, L_c: int):
     return [s for s in range(max(1, lo), min(hi, MAX_STRIDE) + 1) if 2 * s <= L_c]
 
 
+def fold64(v: np.ndarray, L_c: int, sigma: int) -> np.ndarray:
+    """c_sigma[p] for p in [0, sigma) in fp64 (the mean over periods)."""
+    return np.array([v[p:L_c:sigma].mean() for p in range(sigma)])
+
+
 def fold(v: np.ndarray, L_c: int, sigma: int) -> np.ndarray:
     """c_sigma[p] for p in [0, sigma), fp64 then rounded to fp32."""
-    c = np.array([v[p:L_c:sigma].mean() for p in range(sigma)])
-    return c.astype(np.float32)
+    return fold64(v, L_c, sigma).astype(np.float32)
+
+
+def pick(folds: dict, eps: float = EPS_G):
+    """The decision of the search from fp32 folds {sigma: c_sigma}: the
+    smallest argmax phase of each stride, strides scanned ascending, a later
+    stride replacing the best only if its score exceeds best * (1 + eps)
+    (fp32 product). Returns ((sigma, p_g) or None, {sigma: (score, p)})."""
+    best = None
+    b = np.float32(0.0)
+    one_eps = np.float32(1.0 + eps)
+    picks = {}
+    for s in sorted(folds):
+        c = np.asarray(folds[s], dtype=np.float32)
+        p = int(np.argmax(c))          # first (smallest) index of the maximum
+        sc = c[p]
+        picks[s] = (float(sc), p)
+        if sc > np.float32(b * one_eps):
+            best, b = (s, p), sc
+    return best, picks
 
 
 def search(v: np.ndarray, L_c: int, lo: int, hi: int, eps: float = EPS_G):
     """Returns ((sigma, p_g) or None, {sigma: fp32 fold}, {sigma: (score, p)})."""
-    best = None
-    b = np.float32(0.0)
-    one_eps = np.float32(1.0 + eps)
-    folds, picks = {}, {}
-    for s in candidates(lo, hi, L_c):
-        c = fold(v, L_c, s)
-        p = int(np.argmax(c))          # first (smallest) index of the maximum
-        sc = c[p]
-        folds[s] = c
-        picks[s] = (float(sc), p)
-        if sc > np.float32(b * one_eps):
-            best, b = (s, p), sc
+    folds = {s: fold(v, L_c, s) for s in candidates(lo, hi, L_c)}
+    best, picks = pick(folds, eps)
     return best, folds, picks
 
 

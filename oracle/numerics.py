@@ -2,7 +2,7 @@
 
 bf16 is the top 16 bits of an IEEE-754 binary32. Decoding is exact; encoding
 uses round-to-nearest-even, the rounding the kernel's output uses.
-Pinned by tests/test_oracle_numerics.py against torch's own bf16 casts.
+Pinned in tests/test_oracle_core.py against torch's own bf16 casts.
 """
 import numpy as np
 

@@ -146,6 +146,24 @@ def grid_state(op: C.Op, L: int, sigma: int, p: int) -> OpState:
     return OpState(C.OP_GRID, op, sigma=sigma, p=p, cos=cos, g0=g0, L=L)
 
 
+def adopt(st: OpState, sigma=None, p=None, vsel=None, ssel=None) -> OpState:
+    """The op with the given discrete choices in place of its estimated ones:
+    a Grid stride and phase (sigma 0 = no stride, dense fallback), or the
+    selected vertical coordinates / slash offsets. Used when another
+    implementation's choice differs from this one's only inside a tie."""
+    op = st.op
+    if op.kind == C.OP_GRID:
+        if int(sigma) == 0:
+            return OpState(C.OP_DENSE, op, L=st.L)
+        return grid_state(op, st.L, int(sigma), int(p))
+    if op.kind == C.OP_VSLASH:
+        return OpState(C.OP_VSLASH, op, vsel=np.asarray(vsel, dtype=np.int64),
+                       ssel=np.asarray(ssel, dtype=np.int64), L=st.L)
+    if op.kind == C.OP_VERT:
+        return OpState(C.OP_VERT, op, vsel=np.asarray(vsel, dtype=np.int64), L=st.L)
+    raise ValueError(f"op kind {op.kind} has no estimated choice")
+
+
 def choose(cfg: C.HeadCfg, S: int, modality, q_rows, K: np.ndarray, scale=None):
     """Estimation and discrete choices of one head.
 

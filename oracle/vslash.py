@@ -7,7 +7,7 @@ Order: score descending, ties to the smaller index; decided on fp32-rounded
 scores. n >= L_c selects everything.
 
 Token predicate: k in Vset  or  (q - k) in Oset (coordinates of the op).
-Pinned in tests/test_oracle_vslash.py against a sort-based brute force and
+Pinned in tests/test_oracle_core.py against a sort-based brute force and
 the reductions n >= L_c -> dense.
 """
 import numpy as np
@@ -23,11 +23,3 @@ def topk(scores: np.ndarray, n: int, L: int) -> np.ndarray:
     order = np.lexsort((np.arange(L), -x))
     return np.sort(order[:n]).astype(np.int64)
 
-
-def margin(scores: np.ndarray, n: int, L: int) -> float:
-    """Relative gap between the n-th and (n+1)-th largest fp32 scores (inf if none)."""
-    if n >= L or n <= 0:
-        return float("inf")
-    x = np.sort(np.asarray(scores[:L]).astype(np.float64))[::-1]
-    top = max(x[0], 1e-300)
-    return float((x[n - 1] - x[n]) / top)

@@ -31,6 +31,11 @@
 // The running maximum is only moved when a row's block maximum exceeds it by
 // more than RESCALE_SLACK (log2 units): P entries then stay below 2^8, which
 // neither bf16 nor the fp32 sums mind, and the O rescale becomes rare.
+// Each row keeps two sums: l over the fp32 P (for the LSE) and lo over the
+// bf16-rounded P that the PV product actually uses (for O = PV / lo). With
+// lo, O is a convex combination of V rows whatever the rounding of P, so a
+// row dominated by one key is not scaled by that key's rounding error (up to
+// 2^-8 relative, which for |V| of several units exceeds the output bound).
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -216,12 +221,22 @@ __device__ __forceinline__ float xhalf_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+
+// Sum of the 8 bf16 values of a packed P operand, added to acc (v_dot2 with ones).
+__device__ __forceinline__ float sum8(const bf16x8& p, float acc) {
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int x = 0; x < 4; ++x) acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p[2 * x], p[2 * x + 1]}, one, acc, false);
+  return acc;
+}
+
 // Online-softmax step on the scores of one block: P = 2^(s*sc - m) packed to
-// bf16 B operands, row sum into l. m moves (alpha < 1) only when some row's
+// bf16 B operands, row sums into l (fp32 P) and lo (bf16 P). m moves (alpha < 1) only when some row's
 // block maximum passes it by more than RESCALE_SLACK. Branch-free, so that
 // the compiler can interleave it with independent MFMAs.
-__device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m, float& l, bf16x8 (&pb)[4],
-                                              float& alpha) {
+__device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m, float& l, float& lo,
+                                              bf16x8 (&pb)[4], float& alpha) {
   float mx = NEG_BIG;
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt)
@@ -241,13 +256,16 @@ __device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m
       s[kt][x] = p;
       rs += p;
     }
+  float ro = 0.0f;
 #pragma unroll
   for (int stp = 0; stp < 4; ++stp) {
     const int kt = stp >> 1, half = stp & 1;
 #pragma unroll
     for (int x = 0; x < 8; ++x) pb[stp][x] = (__bf16)s[kt][4 * (2 * half + (x >> 2)) + (x & 3)];
+    ro = sum8(pb[stp], ro);
   }
   l = l * alpha + xhalf_sum(rs);
+  lo = lo * alpha + xhalf_sum(ro);
 }
 
 // O^T += V^T P^T; the V^T operand comes from row-major V by transpose reads.
@@ -270,7 +288,7 @@ __device__ __forceinline__ void pv_block(const Stage& st, const bf16x8 (&pb)[4],
 struct WaveState {
   f32x16 o[4];
   bf16x8 qr[8];
-  float m, l;
+  float m, l, lo;
   int qpos, rb, c, h, vlane;
 };
 
@@ -285,14 +303,14 @@ __device__ __forceinline__ bool needs_mask(int e, int rb) { return (e >> (24 + r
 
 // Softmax of one block cut into pieces that can be spread between MFMAs:
 // 0-3 running maximum over 8 scores each, 4 new maximum, 5-36 one
-// exponential each, 37-40 bf16 packing, 41 row sum.
+// exponential each, 37-40 bf16 packing and the bf16 row sum, 41 row sums.
 constexpr int SM_PIECES = 42;
 
 struct SoftmaxState {
-  float mx, m_new, rs;
+  float mx, m_new, rs, ro;
 };
 
-__device__ __forceinline__ void softmax_piece(int pc, f32x16 (&s)[2], float sc, float& m, float& l,
+__device__ __forceinline__ void softmax_piece(int pc, f32x16 (&s)[2], float sc, float& m, float& l, float& lo,
                                               bf16x8 (&pb)[4], float& alpha, SoftmaxState& st) {
   if (pc < 4) {
     const int kt = pc >> 1, x0 = (pc & 1) * 8;
@@ -307,6 +325,7 @@ __device__ __forceinline__ void softmax_piece(int pc, f32x16 (&s)[2], float sc, 
     alpha = fast_exp2(m - st.m_new);
     m = st.m_new;
     st.rs = 0.0f;
+    st.ro = 0.0f;
   } else if (pc < 37) {
     const int e = pc - 5, kt = e >> 4, x = e & 15;
     const float p = fast_exp2(fmaf(s[kt][x], sc, -st.m_new));
@@ -316,8 +335,10 @@ __device__ __forceinline__ void softmax_piece(int pc, f32x16 (&s)[2], float sc, 
     const int stp = pc - 37, kt = stp >> 1, half = stp & 1;
 #pragma unroll
     for (int x = 0; x < 8; ++x) pb[stp][x] = (__bf16)s[kt][4 * (2 * half + (x >> 2)) + (x & 3)];
+    st.ro = sum8(pb[stp], st.ro);
   } else {
     l = l * alpha + xhalf_sum(st.rs);
+    lo = lo * alpha + xhalf_sum(st.ro);
   }
 }
 
@@ -364,10 +385,10 @@ __device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, cons
     }
     const int pe = (i + 1) * SM_PIECES / (NM > 0 ? NM : 1);
 #pragma unroll
-    for (; pc < pe; ++pc) softmax_piece(pc, s_sm, sc, ws.m, ws.l, p_new, alpha, st);
+    for (; pc < pe; ++pc) softmax_piece(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
   }
 #pragma unroll
-  for (; pc < SM_PIECES; ++pc) softmax_piece(pc, s_sm, sc, ws.m, ws.l, p_new, alpha, st);
+  for (; pc < SM_PIECES; ++pc) softmax_piece(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
 }
 
 // Step t. Entries e0..e2 are the union entries t..t+2 (0 past the end): key
@@ -448,7 +469,7 @@ __device__ __forceinline__ void block_loop(WaveState& ws, Stage* stg, const Attn
     qk_block(stg[0], ws.qr, ws.c, ws.h, sa);
     if (needs_mask(e0, ws.rb)) mask_block(stg[0], mask_limit(ws, CAUSAL), ws.h, sa);
     float alpha;
-    softmax_block(sa, sc, ws.m, ws.l, pa, alpha);
+    softmax_block(sa, sc, ws.m, ws.l, ws.lo, pa, alpha);
   }
   if (n > 1 && sel(e1, ws.rb)) qk_block(stg[1], ws.qr, ws.c, ws.h, sb);
   // two steps per trip so that the buffers swap roles without copies
@@ -497,15 +518,18 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
     for (int e = 0; e < 16; ++e) ws.o[dt][e] = 0.0f;
   ws.m = NEG_BIG;
   ws.l = 0.0f;
+  ws.lo = 0.0f;
   if (!hd.causal) block_loop<R, true, false>(ws, stg, a, hd, w, tid);
   else if (hd.kperm) block_loop<R, true, true>(ws, stg, a, hd, w, tid);
   else block_loop<R, false, true>(ws, stg, a, hd, w, tid);
 
   const float m = ws.m, l = ws.l;
   const int qpos = ws.qpos, h = ws.h;
+  // every live row has its own key, so lo > 0 unless this part of a split
+  // row selected nothing (then O, l are 0 and the part weighs nothing)
+  const float inv = ws.lo > 0.0f ? 1.0f / ws.lo : 0.0f;
   if (w.part < 0) {
     if (qpos >= 0) {
-      const float inv = 1.0f / l;
       uint16_t* orow = reinterpret_cast<uint16_t*>(a.o) + (int64_t)qpos * a.o_ss + (int64_t)w.head * a.o_sh;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
@@ -525,7 +549,8 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        float4 t = make_float4(ws.o[dt][4 * i], ws.o[dt][4 * i + 1], ws.o[dt][4 * i + 2], ws.o[dt][4 * i + 3]);
+        float4 t = make_float4(ws.o[dt][4 * i] * inv, ws.o[dt][4 * i + 1] * inv, ws.o[dt][4 * i + 2] * inv,
+                               ws.o[dt][4 * i + 3] * inv);
         *reinterpret_cast<float4*>(po + 32 * dt + 8 * i + 4 * h) = t;
       }
     if (h == 0) {
@@ -536,8 +561,9 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
   }
 }
 
-// Merge the (O, m, l) partials of a split row group in a fixed order:
-// M = max m_p, L = sum l_p 2^(m_p - M), O = sum O_p 2^(m_p - M) / L.
+// Merge the (O, m, l) partials of a split row group in a fixed order; each
+// partial O_p is already normalised by its own bf16-P sum, and weighs
+// w_p = l_p 2^(m_p - M): M = max m_p, L = sum w_p, O = sum w_p O_p / L.
 // Workgroup = the 64 rows of query block blockIdx.y of the group, 4 threads per row.
 __global__ __launch_bounds__(256) void k_combine(AttnArgs a, const SplitRow* splits) {
   const SplitRow sr = splits[blockIdx.x];
@@ -557,8 +583,8 @@ __global__ __launch_bounds__(256) void k_combine(AttnArgs a, const SplitRow* spl
   float L = 0.0f;
   for (int p = 0; p < sr.nparts; ++p) {
     const int64_t pr = (int64_t)(sr.part0 + p) * stride + row;
-    const float wgt = fast_exp2(a.part_ml[pr * 2] - M);
-    L += a.part_ml[pr * 2 + 1] * wgt;
+    const float wgt = a.part_ml[pr * 2 + 1] * fast_exp2(a.part_ml[pr * 2] - M);
+    L += wgt;
     const float4* src = reinterpret_cast<const float4*>(a.part_o + pr * D + quarter * 32);
 #pragma unroll
     for (int x = 0; x < 8; ++x) {

@@ -12,10 +12,11 @@ This module draws random numbers only; it holds none of the method's
 arithmetic. The same tensors feed the HIP path and the CPU oracle.
 
 Structure planted per KV group g (added to Q of every query head of g and
-to K of head g; V stays iid N(0,1) so |O| stays below 8 and bf16 output
-rounding stays inside the 2e-2 bound):
+to K of head g; to V only where v_embed is set):
   * slot embedding  E_g[s] ~ amp * N(0, I)  at video tokens whose video-local
-    index is s mod sigma_g  (the same-spatial-slot lines of the grid);
+    index is s mod sigma_g  (the same-spatial-slot lines of the grid); with
+    v_embed the same embedding is added to V as well (Q, K and V share the
+    per-position embedding, so outputs reach |O| of several units);
   * one line slot p*_g: keys of that slot get  line_k * w_g  and every video
     query gets  line_q * w_g  (the vertical lines of the grid);
   * text: a causal exponential-filter (AR(1)-like) bias of amplitude
@@ -44,6 +45,7 @@ class Structure:
     text_rho: float = 0.95
     sink_frac: float = 0.0
     line_slot: Optional[List[int]] = None   # filled by make_workload (seeded)
+    v_embed: bool = False             # add the slot embedding to V too
 
 
 @dataclass
@@ -118,6 +120,8 @@ def make_qkv(wl: Workload, device="cpu", dtype=torch.bfloat16):
                 e = _periodic(E, v0 % sig, b - a)
                 K[a:b, g] += e
                 Q[a:b, g * G:(g + 1) * G] += e[:, None, :]
+                if st.v_embed:
+                    V[a:b, g] += e
                 first = (p_star - v0) % sig
                 K[a + first:b:sig, g] += st.line_k * w
                 Q[a:b, g * G:(g + 1) * G] += st.line_q * w

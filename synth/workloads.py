@@ -31,10 +31,11 @@ def _line_slots(rng, sigmas):
 
 
 def config0() -> Workload:
-    """4096 = 64 text + 16 frames x 252; 2 query heads / 1 KV head; Grid(frame 252)."""
+    """4096 = 64 text + 16 frames x 252; 2 query heads / 1 KV head; Grid(frame 252);
+    the slot embedding on Q, K and V."""
     rng = _rng(0)
     mod = _layout([(0, 64), (1, 16 * 252)])
-    st = Structure(sigma=[252], amp=2.0)
+    st = Structure(sigma=[252], amp=2.0, v_embed=True)
     st.line_slot = _line_slots(rng, st.sigma)
     heads = [C.global_head(C.grid_frame(252)) for _ in range(2)]
     return Workload("cfg0_grid_4k", 4096, 2, 1, mod, heads, st, SEED0 + 0, frame=252)
@@ -42,11 +43,12 @@ def config0() -> Workload:
 
 def config1() -> Workload:
     """32768 = 128 text + 128 frames x 255; 28/4; stride 255+U{-4..4} per KV group;
-    per-head pattern drawn from {Grid(window), A-shape(128,1024), VS(1000,1024)}."""
+    per-head pattern drawn from {Grid(window), A-shape(128,1024), VS(1000,1024)};
+    the slot embedding on Q, K and V."""
     rng = _rng(1)
     mod = _layout([(0, 128), (1, 128 * 255)])
     sig = [255 + int(rng.integers(-4, 5)) for _ in range(4)]
-    st = Structure(sigma=sig, amp=2.0)
+    st = Structure(sigma=sig, amp=2.0, v_embed=True)
     st.line_slot = _line_slots(rng, sig)
     choices = [C.grid_window(255), C.ashape(128, 1024), C.vslash(1000, 1024)]
     heads = [C.global_head(choices[int(rng.integers(0, 3))]) for _ in range(28)]

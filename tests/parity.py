@@ -1,33 +1,30 @@
-"""Parity helpers: run the HIP path through the C-ABI and compare it with the
-oracle on the same seeded inputs (test infrastructure).
-
-Layered comparison (discrete choices first, so bit-exactness of the block
-index is not hostage to fp32-vs-fp64 noise):
-  1. scores   GPU v/u/fold vs oracle fp64, relative error on significant entries;
-  2. choices  Grid (sigma, phase) and VS/VERT selections equal the oracle's
-              (a mismatch is accepted only where the oracle's own decision
-              margin is below the tie tolerance; such heads are reported and
-              their blocks/outputs checked for validity only);
-  3. blocks   permutations and CSR bit-exact against the oracle's closed forms;
-  4. outputs  O max-abs <= 2e-2 (bf16), LSE |diff| <= 1e-3 * max(1, |LSE|).
+"""Parity driver: run the HIP path through the C-ABI, export what it chose and
+computed, and compare every checked head with the oracle (test
+infrastructure). The per-head comparison and its five layers are in
+parity_core.py; this module holds the GPU side and the fan-out of heads over
+worker processes for the full-size workloads.
 """
 from __future__ import annotations
 
+import multiprocessing as mp
+import os
+import shutil
 import sys
+import tempfile
+import time
+from concurrent.futures import ProcessPoolExecutor
 from dataclasses import dataclass, field
 
 import numpy as np
 import torch
 
-from oracle import attention as OA
+import parity_core as PC
+from oracle import layout as OL
 from oracle import numerics as ON
-from oracle import plan as OP
 from synth import config as C
 
-O_TOL = 2e-2
-LSE_TOL = 1e-3
-SCORE_RTOL = 2e-3
-TIE_RTOL = 1e-4
+O_TOL, LSE_TOL, SCORE_RTOL, TIE_RTOL = PC.O_TOL, PC.LSE_TOL, PC.SCORE_RTOL, PC.TIE_RTOL
+ROWS_PER_HEAD = 4096
 
 
 def say(*a):
@@ -35,21 +32,30 @@ def say(*a):
     sys.stdout.flush()
 
 
-def slot_of(key):
-    if key == "g":
-        return 0
-    if key[0] in ("q", "i"):
-        return key[1]
-    return 8 + key[1] * 8 + key[2]
-
-
 @dataclass
 class Report:
     ties: list = field(default_factory=list)
+    heads: list = field(default_factory=list)
     max_o: float = 0.0
+    max_o_excess: float = 0.0
     max_lse: float = 0.0
+    score_err: float = 0.0
     rows: int = 0
     nnz: dict = field(default_factory=dict)
+
+    def add(self, r):
+        self.heads.append(r["head"])
+        self.ties += [(r["head"],) + tuple(t) for t in r["ties"]]
+        self.max_o = max(self.max_o, r["max_o"])
+        self.max_o_excess = max(self.max_o_excess, r["max_o_excess"])
+        self.max_lse = max(self.max_lse, r["max_lse"])
+        self.score_err = max(self.score_err, r["score_err"])
+        self.rows += r["rows"]
+        self.nnz[r["head"]] = r["nnz"]
+
+    def line(self):
+        return (f"heads={len(self.heads)} rows={self.rows} ties={self.ties} score_err={self.score_err:.2e} "
+                f"max|dO|={self.max_o:.3g} (excess {self.max_o_excess:.3g}) lse={self.max_lse:.3g}")
 
 
 def run_gpu(ctx, S, Hq, Hkv, modality, heads, q, k, v):
@@ -63,175 +69,137 @@ def run_gpu(ctx, S, Hq, Hkv, modality, heads, q, k, v):
     return plan, o, lse
 
 
-def _rel_err(gpu, ref):
-    ref = np.asarray(ref, dtype=np.float64)
-    gpu = np.asarray(gpu, dtype=np.float64)
-    if ref.size == 0:
-        return 0.0
-    big = np.abs(ref) >= 1e-6 * max(np.abs(ref).max(), 1e-300)
-    if not big.any():
-        return 0.0
-    return float((np.abs(gpu - ref)[big] / np.abs(ref)[big]).max())
-
-
-def compare_head(plan, h, hp: OP.HeadPlan, rep: Report, exact_choices=True):
-    """Steps 1-3 for one head. Returns True if the block index was compared exactly."""
-    tied = False
-    for key, est in hp.est.items():
-        s = slot_of(key)
-        gv = plan.export(h, "v", s)
-        assert len(gv) == est.L_c, (h, key, len(gv), est.L_c)
-        if est.L_c == 0:
-            # a cross pair whose key modality has no token before the final
-            # query rows: nothing to select, the library runs no estimation
-            continue
-        ev = _rel_err(gv, est.v)
-        assert ev <= SCORE_RTOL, f"head {h} {key}: v rel err {ev}"
-        if est.u is not None and hp.ops[key].op.kind == C.OP_VSLASH:
-            gu = plan.export(h, "u", s)
-            eu = _rel_err(gu, est.u)
-            assert eu <= SCORE_RTOL, f"head {h} {key}: u rel err {eu}"
-        gl = plan.export(h, "est_lse", s)
-        assert np.abs(gl - est.lse).max() <= 1e-3 * max(1.0, np.abs(est.lse).max()), (h, key)
-    for key, st in hp.ops.items():
-        s = slot_of(key)
-        if st.op.kind == C.OP_GRID:
-            prm = plan.export(h, "params", s)
-            got = (int(prm[0]), int(prm[1]))
-            want = (st.sigma, st.p) if st.kind == C.OP_GRID else (0, 0)
-            if got != want:
-                folds = hp.folds[key]
-                if want[0] and got[0] in folds and want[0] in folds:
-                    a, b = folds[want[0]].max(), folds[got[0]].max()
-                    gap = abs(float(a) - float(b)) / max(float(a), 1e-30)
-                    if gap < TIE_RTOL:
-                        tied = True
-                        rep.ties.append((h, key, want, got))
-                        continue
-                raise AssertionError(f"head {h} {key}: grid choice gpu {got} oracle {want}")
-        if st.kind in (C.OP_VSLASH, C.OP_VERT):
-            gsel = plan.export(h, "vsel", s)
-            if not np.array_equal(gsel, st.vsel):
-                tied |= _tie_ok(hp.est[key].v, gsel, st.vsel, f"head {h} {key} vsel")
-                rep.ties.append((h, key, "vsel"))
-            if st.kind == C.OP_VSLASH:
-                gss = plan.export(h, "ssel", s)
-                if not np.array_equal(gss, st.ssel):
-                    tied |= _tie_ok(hp.est[key].u, gss, st.ssel, f"head {h} {key} ssel")
-                    rep.ties.append((h, key, "ssel"))
-    gq = plan.export(h, "qperm")
-    gk = plan.export(h, "kperm")
-    if not tied:
-        assert np.array_equal(gq, hp.qperm), f"head {h}: qperm differs"
-        assert np.array_equal(gk, hp.kperm), f"head {h}: kperm differs"
-        rp = plan.export(h, "row_ptr")
-        col = plan.export(h, "col_idx")
-        want_rp = np.concatenate([[0], np.cumsum([len(b) for b in hp.blocks])])
-        assert np.array_equal(rp, want_rp), f"head {h}: row_ptr differs"
-        assert np.array_equal(col, np.concatenate(hp.blocks)), f"head {h}: col_idx differs"
-        rep.nnz[h] = len(col)
-    return not tied
-
-
-def _tie_ok(score, gsel, osel, what):
-    """A different selection is valid only if every swapped element is within
-    the tie tolerance of the selection threshold (oracle fp64 scores)."""
-    x = np.asarray(score, dtype=np.float64)
-    assert len(gsel) == len(osel), f"{what}: size {len(gsel)} vs {len(osel)}"
-    only_g = np.setdiff1d(gsel, osel)
-    only_o = np.setdiff1d(osel, gsel)
-    thr = x[osel].min() if len(osel) else 0.0
-    scale = max(x.max(), 1e-300)
-    bad = [(i, x[i]) for i in np.concatenate([only_g, only_o]) if abs(x[i] - thr) > TIE_RTOL * scale]
-    assert not bad, f"{what}: selection differs beyond ties: {bad[:5]}"
-    return True
-
-
-def compare_outputs(h, hp, Q, K, V, kvh, O, LSE, rows, rep: Report):
-    Oo, Lo = OA.head_rows(hp, Q[:, h], K[:, kvh], V[:, kvh], rows)
-    eo = float(np.abs(O[rows, h] - Oo).max())
-    el = float((np.abs(LSE[h, rows] - Lo) / np.maximum(1.0, np.abs(Lo))).max())
-    rep.max_o = max(rep.max_o, eo)
-    rep.max_lse = max(rep.max_lse, el)
-    rep.rows += len(rows)
-    assert eo <= O_TOL, f"head {h}: max |O - O_oracle| = {eo}"
-    assert el <= LSE_TOL, f"head {h}: LSE rel err {el}"
+def export_head(plan, h, cfg, S, modality):
+    """Everything the comparison needs from the library for one head."""
+    gpu = dict(qperm=plan.export(h, "qperm"), kperm=plan.export(h, "kperm"),
+               row_ptr=plan.export(h, "row_ptr"), col_idx=plan.export(h, "col_idx"), slots={})
+    for key, op in PC.op_keys(cfg, S, modality):
+        s = PC.slot_of(key)
+        d = dict(params=plan.export(h, "params", s), v=plan.export(h, "v", s), est_lse=plan.export(h, "est_lse", s))
+        if op.kind == C.OP_GRID:
+            d["fold"] = plan.export(h, "fold", s)
+        else:
+            d["vsel"] = plan.export(h, "vsel", s)
+        if op.kind == C.OP_VSLASH:
+            d["u"] = plan.export(h, "u", s)
+            d["ssel"] = plan.export(h, "ssel", s)
+        gpu["slots"][key] = d
+    return gpu
 
 
 def full_check(ctx, S, Hq, Hkv, modality, heads, q, k, v, rows=None, heads_to_check=None):
-    """GPU run + oracle plans + layered comparison. q/k/v: CUDA bf16 tensors."""
+    """GPU run + layered comparison of every head (or heads_to_check) in this
+    process, on all rows or the given rows. q/k/v: CUDA bf16 tensors."""
     plan, o, lse = run_gpu(ctx, S, Hq, Hkv, modality, heads, q, k, v)
     Q, K, V = (ON.torch_bf16_to_f64(t) for t in (q, k, v))
     O = ON.torch_bf16_to_f64(o)
     LSE = lse.cpu().double().numpy()
     G = Hq // Hkv
+    rr = np.arange(S) if rows is None else np.asarray(rows, dtype=np.int64)
     rep = Report()
     try:
         for h in (heads_to_check if heads_to_check is not None else range(Hq)):
-            hp = OP.plan_head(heads[h], S, modality, lambda r, h=h: Q[r, h], K[:, h // G])
-            exact = compare_head(plan, h, hp, rep)
-            if exact:
-                rr = np.arange(S) if rows is None else rows
-                compare_outputs(h, hp, Q, K, V, h // G, O, LSE, rr, rep)
+            gpu = export_head(plan, h, heads[h], S, modality)
+            r = PC.check_head(h, heads[h], S, modality, lambda x, h=h: Q[x, h], K[:, h // G], V[:, h // G], gpu,
+                              rr, O[rr, h], LSE[h, rr])
+            rep.add(r)
     finally:
         plan.destroy()
     return rep
 
 
-def sample_rows(S, modality, rng, n_uniform=64, last=64, around=8):
-    """Stratified query rows: the last rows, rows on both sides of every
-    modality boundary, and uniform rows (seeded)."""
-    rows = set(range(max(0, S - last), S))
-    if modality is not None:
-        cut = np.nonzero(np.diff(np.asarray(modality).astype(np.int16)))[0] + 1
-        for c in cut[:64]:
-            rows.update(range(max(0, c - around), min(S, c + around)))
-    rows.update(rng.choice(S, size=min(n_uniform, S), replace=False).tolist())
-    return np.array(sorted(rows), dtype=np.int64)
+def _workers():
+    """Oracle worker processes: the host's cores, at most 12 (the GPU machine
+    grants one GPU's share of its CPUs; this process keeps the GPU)."""
+    n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    return max(1, min(12, n))
 
 
-def sampled_check(ctx, wl, q, k, v, heads_to_check, rows_extra=None, seed=0):
-    """Full-size parity: every head's scores, choices, permutations and block
-    index are compared in full; O/LSE on stratified sampled rows (including
-    each Grid head's first horizontal-line rows)."""
-    plan, o, lse = run_gpu(ctx, wl.S, wl.Hq, wl.Hkv, wl.modality, wl.heads, q, k, v)
-    G = wl.Hq // wl.Hkv
-    rng = np.random.default_rng(seed)
-    base_rows = sample_rows(wl.S, wl.modality, rng)
-    kv_cache = {}
+def _scratch_dir():
+    for base in ("/dev/shm", tempfile.gettempdir()):
+        try:
+            st = os.statvfs(base)
+            if st.f_bavail * st.f_frsize > (8 << 30):
+                return tempfile.mkdtemp(prefix="mmi_parity_", dir=base)
+        except OSError:
+            continue
+    return tempfile.mkdtemp(prefix="mmi_parity_")
 
-    def kv(g):
-        if g not in kv_cache:
-            kv_cache.clear()
-            kv_cache[g] = (ON.torch_bf16_to_f64(k[:, g]), ON.torch_bf16_to_f64(v[:, g]))
-        return kv_cache[g]
 
+def _bits(t):
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def run_tasks(tasks, workers=None, t0=None):
+    """parity_core.run_task over the tasks, in fresh oracle worker processes
+    (spawn: they import numpy and the oracle only, never the GPU), with one
+    BLAS thread each. Returns the merged Report."""
+    t0 = time.time() if t0 is None else t0
     rep = Report()
+    nw = workers or _workers()
+    if nw <= 1 or len(tasks) <= 1:
+        for t in tasks:
+            rep.add(PC.run_task(t))
+        return rep
+    env_old = {x: os.environ.get(x) for x in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")}
+    for x in env_old:
+        os.environ[x] = "1"
     try:
-        for h in heads_to_check:
-            qh = q[:, h]
-
-            def q_rows(r, qh=qh):
-                return ON.torch_bf16_to_f64(qh[torch.as_tensor(np.asarray(r), device=qh.device)])
-
-            K, V = kv(h // G)
-            hp = OP.plan_head(wl.heads[h], wl.S, wl.modality, q_rows, K)
-            if not compare_head(plan, h, hp, rep):
-                continue
-            rows = base_rows
-            if hp.qperm is not None and hp.nbq:
-                lastblk = hp.qperm[(hp.nbq - 1) * OP.B:hp.nbq * OP.B]
-                rows = np.union1d(rows, lastblk[lastblk >= 0][:8])
-            Oo, Lo = OA.head_rows(hp, q_rows, K, V, rows)
-            Og = ON.torch_bf16_to_f64(o[torch.as_tensor(rows, device=o.device), h])
-            Lg = lse[h, torch.as_tensor(rows, device=lse.device)].cpu().double().numpy()
-            eo = float(np.abs(Og - Oo).max())
-            el = float((np.abs(Lg - Lo) / np.maximum(1.0, np.abs(Lo))).max())
-            rep.max_o = max(rep.max_o, eo)
-            rep.max_lse = max(rep.max_lse, el)
-            rep.rows += len(rows)
-            assert eo <= O_TOL, f"head {h}: max |O - O_oracle| = {eo}"
-            assert el <= LSE_TOL, f"head {h}: LSE rel err {el}"
+        with ProcessPoolExecutor(max_workers=min(nw, len(tasks)), mp_context=mp.get_context("spawn")) as ex:
+            for r in ex.map(PC.run_task, tasks):
+                rep.add(r)
+                say(f"  [parity] head {r['head']}: nnz {r['nnz']} ties {r['ties']} "
+                    f"|dO| {r['max_o']:.3g} score {r['score_err']:.2e} ({time.time() - t0:.0f} s)")
     finally:
-        plan.destroy()
+        for x, val in env_old.items():
+            if val is None:
+                os.environ.pop(x, None)
+            else:
+                os.environ[x] = val
     return rep
+
+
+def sampled_check(ctx, wl, q, k, v, heads_to_check, n_rows=ROWS_PER_HEAD, seed=0, workers=None,
+                  max_hline_blocks=None):
+    """Full-size parity: the GPU plan of the whole layer, then for every head
+    in heads_to_check all five layers (scores, choices re-derived, block index
+    bit-exact, choices against the oracle with ties re-checked under the
+    GPU's choice, O/LSE) on n_rows stratified rows per head. Heads are
+    spread over oracle worker processes, started fresh (spawn): they import
+    numpy and the oracle only and never touch the GPU; K and V reach them
+    through bf16 bit files, each head's query and output rows through the
+    task itself."""
+    S, Hq, Hkv = wl.S, wl.Hq, wl.Hkv
+    G = Hq // Hkv
+    t0 = time.time()
+    plan, o, lse = run_gpu(ctx, S, Hq, Hkv, wl.modality, wl.heads, q, k, v)
+    tmp = _scratch_dir()
+    tasks = []
+    try:
+        path_k, path_v = os.path.join(tmp, "k.npy"), os.path.join(tmp, "v.npy")
+        np.save(path_k, _bits(k.transpose(0, 1)))
+        np.save(path_v, _bits(v.transpose(0, 1)))
+        mod = OL.modality_array(S, wl.modality)
+        T = OL.positions_of(mod)
+        est_rows = {"g": OL.global_rows(S)}
+        est_rows.update({m: OL.final_run_rows(T[m]) for m in T})
+        for h in heads_to_check:
+            cfg = wl.heads[h]
+            gpu = export_head(plan, h, cfg, S, wl.modality)
+            rows = PC.sample_rows(S, wl.modality, cfg, gpu, n_target=n_rows, seed=seed * 1000 + h,
+                                  max_hline_blocks=max_hline_blocks)
+            qpos = np.union1d(rows, np.concatenate(list(est_rows.values())))
+            dev = torch.as_tensor(qpos, device=q.device)
+            drow = torch.as_tensor(rows, device=q.device)
+            tasks.append(dict(h=h, g=h // G, cfg=cfg, S=S, modality=wl.modality, gpu=gpu, q_pos=qpos,
+                              q_bits=_bits(q[dev, h]), rows=rows, o_bits=_bits(o[drow, h]),
+                              lse=lse[h, drow].cpu().double().numpy(), path_k=path_k, path_v=path_v))
+        plan.destroy()
+        plan = None
+        tasks.sort(key=lambda t: t["g"])
+        say(f"  [parity] GPU plan, exports and row gathers: {time.time() - t0:.1f} s, {len(tasks)} heads")
+        return run_tasks(tasks, workers, t0)
+    finally:
+        if plan is not None:
+            plan.destroy()
+        shutil.rmtree(tmp, ignore_errors=True)

@@ -23,30 +23,20 @@ def ctx():
     c.close()
 
 
-def _first_of_each_kind(wl, limit):
-    seen, out = set(), []
-    for h, cfg in enumerate(wl.heads):
-        key = (cfg.kind, cfg.op.kind)
-        if key not in seen:
-            seen.add(key)
-            out.append(h)
-    for h in range(wl.Hq):
-        if len(out) >= limit:
-            break
-        if h not in out:
-            out.append(h)
-    return sorted(out[:limit])
-
-
-@pytest.mark.parametrize("cid,nheads", [(1, 28), (2, 12), (3, 8), (4, 5)])
-def test_workload_parity(ctx, cid, nheads):
+@pytest.mark.parametrize("cid", [0, 1, 2, 3, 4])
+def test_workload_parity(ctx, cid):
+    """Every head of the workload: scores, choices re-derived from the GPU's
+    scores, choices against the oracle (a tie re-checked under the GPU's
+    choice), permutations and block index bit-exact, O/LSE on all rows (4K
+    and 32K) or 4096 stratified rows per head (128K, 256K, 1M)."""
     wl = workloads.by_id(cid)
-    heads = _first_of_each_kind(wl, nheads)
-    say(f"[gpu] workload {wl.name} S={wl.S} heads {heads}")
+    say(f"[gpu] workload {wl.name} S={wl.S} all {wl.Hq} heads")
     q, k, v = generate.make_qkv(wl, "cuda")
-    rep = sampled_check(ctx, wl, q, k, v, heads)
-    say(f"  rows={rep.rows} ties={rep.ties} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g} nnz={rep.nnz}")
-    assert len(rep.ties) <= max(1, len(heads) // 4)
+    n_rows = wl.S if cid <= 1 else 4096
+    rep = sampled_check(ctx, wl, q, k, v, list(range(wl.Hq)), n_rows=n_rows)
+    say("  " + rep.line() + f" nnz={rep.nnz}")
+    assert sorted(rep.heads) == list(range(wl.Hq))
+    assert rep.rows >= wl.Hq * min(n_rows, wl.S)
 
 
 def _union_totals(plan, h, R=4, strides=(1, 2, 4, 8)):
@@ -90,7 +80,7 @@ def test_row_group_stride_choice(ctx):
         plan.destroy()
     rows = np.unique(np.concatenate([np.arange(S - 64, S), np.random.default_rng(1).choice(S, 256, replace=False)]))
     rep = full_check(ctx, S, 2, 1, None, heads, q, k, v, rows=rows)
-    say(f"  ties={rep.ties} max|dO|={rep.max_o:.3g}")
+    say("  " + rep.line())
 
 
 def expected_union(rp, col, qperm, kperm, S, R, rho, ngroups, causal=True):
@@ -157,8 +147,7 @@ def test_qboundary_grid_1m(ctx):
     say(f"[gpu] Q-Boundary Grid on {wl.name}")
     q, k, v = generate.make_qkv(wl, "cuda")
     rep = sampled_check(ctx, wl, q, k, v, [0, 27])
-    say(f"  rows={rep.rows} ties={rep.ties} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g} nnz={rep.nnz}")
-    assert len(rep.ties) <= 1
+    say("  " + rep.line() + f" nnz={rep.nnz}")
 
 
 def test_natten_video(ctx):
@@ -170,7 +159,7 @@ def test_natten_video(ctx):
     say(f"[gpu] {wl.name} grid {wl.extra['grid']} tile {wl.extra['tile']}")
     q, k, v = generate.make_qkv(wl, "cuda")
     rep = sampled_check(ctx, wl, q, k, v, [0, 23])
-    say(f"  rows={rep.rows} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g} nnz={rep.nnz}")
+    say("  " + rep.line() + f" nnz={rep.nnz}")
     assert not rep.ties
     # row groups: the stride with the smallest total union among 1, 2, 4, 8, the
     # tiles of a tile row (10) and of a tile layer (120); unions bit-exact
@@ -198,8 +187,8 @@ def test_natten_video(ctx):
 def test_max_sequence_length(ctx):
     """The largest supported length, S = 2^21 (2,097,152 tokens): A-shape and
     Grid heads on a text + video layout with 256-token frames, block index
-    bit-exact and O/LSE on sampled rows (one head per oracle pass, about a
-    minute each on the host)."""
+    bit-exact and O/LSE on 2048 sampled rows per head (16 of the Grid head's
+    horizontal-line blocks, each of which reads up to every key)."""
     S, F = 1 << 21, 256
     mod = np.ones(S, np.uint8)
     mod[:512] = 0
@@ -208,8 +197,7 @@ def test_max_sequence_length(ctx):
     heads = [C.global_head(C.ashape(128, 4096)), C.global_head(C.grid_window(F))]
     wl = Workload("max_2m", S, 2, 1, mod, heads, st, 20250416 + 21, frame=F)
     q, k, v = generate.make_qkv(wl, "cuda")
-    for h in (0, 1):
-        say(f"[gpu] S = {S}, head {h}")
-        rep = sampled_check(ctx, wl, q, k, v, [h])
-        say(f"  rows={rep.rows} ties={rep.ties} max|dO|={rep.max_o:.3g} lse={rep.max_lse:.3g} nnz={rep.nnz}")
-        assert not rep.ties
+    say(f"[gpu] S = {S}, heads 0 and 1")
+    rep = sampled_check(ctx, wl, q, k, v, [0, 1], n_rows=2048, max_hline_blocks=16)
+    say("  " + rep.line() + f" nnz={rep.nnz}")
+    assert not rep.ties
