@@ -46,6 +46,9 @@ extern "C" {
 #define MMI_LAST_Q 64          /* estimation rows, Section 4.1 (last_q = 64) */
 #define MMI_MAX_STRIDE 1024    /* Grid max stride, Appendix C.5 table */
 #define MMI_MAX_SEQ (1 << 21)  /* largest supported S (2,097,152 tokens) */
+/* Device scratch of mmi_attention_noalloc: a static array of this many bytes
+ * that each GPU the library runs on holds until the process ends. */
+#define MMI_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
 
 /* status codes */
 #define MMI_OK 0
@@ -167,7 +170,8 @@ typedef struct mmi_head_stats {
 } mmi_head_stats;
 
 /* Stage durations of a plan, from HIP events recorded on the plan's stream
- * (Section 4.6 / Appendix E report latency including the index building).
+ * (Section 4.5 "Latency" and Appendix E "Latency Breakdown" report latency
+ * including the index building).
  * create_* cover mmi_plan_create, attn/combine the last mmi_plan_execute. */
 typedef struct mmi_plan_timing {
   float est_ms;        /* estimation passes (row LSE, column/diagonal scores) */
@@ -178,6 +182,7 @@ typedef struct mmi_plan_timing {
   int64_t computed_blocks;  /* selected 64x64 blocks over all heads */
   int64_t work_items;
   int64_t loaded_blocks;    /* K/V blocks staged by the attention kernel (union entries of all row groups) */
+  int64_t device_bytes;     /* device memory the plan holds (its buffers, before allocator rounding) */
 } mmi_plan_timing;
 
 /* export kinds for mmi_plan_export (host copies; the call synchronises) */
@@ -243,6 +248,23 @@ int mmi_plan_destroy(mmi_plan* plan);
 int mmi_attention(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* cfgs,
                   const void* q, const void* k, const void* v, void* o, float* lse,
                   void* stream);
+
+/* mmi_attention for callers that cannot allocate device memory (serving
+ * loops, harnesses that forbid allocation): the same plan and kernels, but
+ * every device buffer of the plan (estimation scores, permutations, block
+ * index, work list, split partials) is carved from the library's static
+ * scratch of MMI_NOALLOC_SCRATCH_BYTES on the context's device. The call
+ * makes no hipMalloc, hipFree, hipHostMalloc or event creation (host heap
+ * memory only for the plan's host-side tables) and returns after its work on
+ * `stream` has finished. Results are bitwise those of mmi_attention.
+ * Returns MMI_ERR_UNSUPPORTED, without writing o or lse, when the plan needs
+ * more than the scratch (the message names the limit; mmi_plan_timing_get's
+ * device_bytes tells a plan's need). Calls on one device are serialised by
+ * the library; the scratch keeps the last call's contents, and every buffer
+ * a call reads is written earlier in that same call. */
+int mmi_attention_noalloc(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* cfgs,
+                          const void* q, const void* k, const void* v, void* o, float* lse,
+                          void* stream);
 
 /* Every causal block of every head through the same kernel: the dense
  * causal attention baseline on the same GPU. */

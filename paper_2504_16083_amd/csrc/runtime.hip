@@ -98,6 +98,30 @@ class Allocator {
 
 }  // namespace mmi
 
+// ------------------------------------------------------------------ no-allocation scratch
+// Device memory of mmi_attention_noalloc: one static array, which every GPU
+// the library runs on holds (its own copy) until the process ends. Host code
+// never passes the array's name as an address: its address on each device
+// comes from hipGetSymbolAddress, taken once per device when the first
+// context on that device is created.
+static __device__ __align__(256) uint8_t scratch[MMI_NOALLOC_SCRATCH_BYTES];
+
+namespace mmi {
+constexpr int MAX_DEVICES = 64;
+static std::mutex g_scratch_mu;                      // guards g_scratch_ptr
+static uint8_t* g_scratch_ptr[MAX_DEVICES] = {};     // address of `scratch` on each device
+static std::mutex g_scratch_call_mu[MAX_DEVICES];    // one no-allocation call at a time per device
+
+static void scratch_setup(int device) {              // device is current
+  if (device >= MAX_DEVICES) return;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[device]) return;
+  void* ptr = nullptr;
+  HIPCHK(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+  g_scratch_ptr[device] = static_cast<uint8_t*>(ptr);
+}
+}  // namespace mmi
+
 struct mmi_ctx {
   int device = 0;
   int chunk_blocks = 64;           // smallest work-item length (union entries)
@@ -168,6 +192,9 @@ struct mmi_plan {
   int64_t gnnz_all = 0;
   bool executed = false;
   std::vector<int> rowset_n;
+  int64_t device_bytes = 0;       // device memory the plan holds
+  uint8_t* scratch = nullptr;     // non-null: buffers come from the no-allocation scratch
+  size_t scratch_used = 0;
 };
 
 namespace mmi {
@@ -175,9 +202,25 @@ namespace mmi {
 template <typename T>
 static T* dalloc(mmi_plan* P, size_t count) {
   size_t bytes = std::max<size_t>(count, 1) * sizeof(T);
+  if (P->scratch) {                      // bump allocation inside the static scratch
+    const size_t off = (P->scratch_used + 255) & ~(size_t)255;
+    if (bytes > MMI_NOALLOC_SCRATCH_BYTES || off > MMI_NOALLOC_SCRATCH_BYTES - bytes)
+      fail(MMI_ERR_UNSUPPORTED,
+           "the plan needs more than the %zu bytes of no-allocation scratch (S = %d, Hq = %d); "
+           "use mmi_attention", (size_t)MMI_NOALLOC_SCRATCH_BYTES, P->S, P->Hq);
+    P->scratch_used = off + bytes;
+    P->device_bytes = (int64_t)P->scratch_used;
+    return reinterpret_cast<T*>(P->scratch + off);
+  }
   void* p = P->ctx->alloc.get(bytes);
   P->bufs.push_back({p, bytes});
+  P->device_bytes += (int64_t)bytes;
   return reinterpret_cast<T*>(p);
+}
+
+// Stage boundary event (plans in scratch mode create no events).
+static void mark(mmi_plan* P, int i, hipStream_t st) {
+  if (P->ev[i]) HIPCHK(hipEventRecord(P->ev[i], st));
 }
 
 // Several host arrays sent as one device allocation and one copy (fewer
@@ -738,7 +781,8 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
 
   // estimation -> choices
   const Tensor tq{q, p.q_stride_s, p.q_stride_h}, tk{k, p.k_stride_s, p.k_stride_h};
-  for (auto& e : P->ev) HIPCHK(hipEventCreate(&e));
+  if (!P->scratch)
+    for (auto& e : P->ev) HIPCHK(hipEventCreate(&e));
   RowSet* d_rs = nullptr;
   EstJob* d_jobs = nullptr;
   GridJob* d_g = nullptr;
@@ -755,14 +799,14 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
     pk.add(qjobs, d_qj);
     send(P, pk);
   }
-  HIPCHK(hipEventRecord(P->ev[0], st));
+  mark(P, 0, st);
   HIPCHK(launch_est_lse(d_rs, (int)bd.rowsets.size(), bd.max_chunks, tq, tk, bd.chunk_keys, st));
   HIPCHK(launch_est_scores(d_jobs, (int)bd.jobs.size(), bd.max_tiles, d_rs, tq, tk, st));
   HIPCHK(launch_est_udiag(d_jobs, (int)bd.jobs.size(), bd.max_L, st));
-  HIPCHK(hipEventRecord(P->ev[1], st));
+  mark(P, 1, st);
   HIPCHK(launch_grid_search(d_g, (int)bd.gjobs.size(), bd.max_cands, st));
   HIPCHK(launch_topk(d_t, (int)bd.tjobs.size(), st));
-  HIPCHK(hipEventRecord(P->ev[2], st));
+  mark(P, 2, st);
 
   // permutations, key summaries, block counts
   HIPCHK(launch_perms(P->d_heads, p.Hq, P->d_ops, g, bd.d_tpos, S, max_slots, st));
@@ -785,13 +829,22 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   for (const auto& hd : P->heads) groups_all += (hd.nbq + R - 1) / R;
   const int split_above_avg = groups_all >= ctx->items_per_layer ? 6 : 0;
   HIPCHK(launch_blocks_scan(P->d_heads, p.Hq, chunk, items_per_head, split_above_avg, d_tot, st));
-  if (ctx->pinned_n < ntot) {
-    if (ctx->pinned) HIPCHK(hipHostFree(ctx->pinned));
-    ctx->pinned = nullptr;
-    HIPCHK(hipHostMalloc((void**)&ctx->pinned, sizeof(int64_t) * ntot));
-    ctx->pinned_n = ntot;
+  std::vector<int64_t> tot_host;
+  const int64_t* tot = nullptr;
+  if (P->scratch) {                      // pageable host copy: no pinned allocation
+    tot_host.resize(ntot);
+    HIPCHK(hipMemcpyAsync(tot_host.data(), d_tot, sizeof(int64_t) * ntot, hipMemcpyDeviceToHost, st));
+    tot = tot_host.data();
+  } else {
+    if (ctx->pinned_n < ntot) {
+      if (ctx->pinned) HIPCHK(hipHostFree(ctx->pinned));
+      ctx->pinned = nullptr;
+      HIPCHK(hipHostMalloc((void**)&ctx->pinned, sizeof(int64_t) * ntot));
+      ctx->pinned_n = ntot;
+    }
+    HIPCHK(hipMemcpyAsync(ctx->pinned, d_tot, sizeof(int64_t) * ntot, hipMemcpyDeviceToHost, st));
+    tot = ctx->pinned;
   }
-  HIPCHK(hipMemcpyAsync(ctx->pinned, d_tot, sizeof(int64_t) * ntot, hipMemcpyDeviceToHost, st));
   HIPCHK(hipStreamSynchronize(st));
 
   // sizes known: column pools, work items, partials
@@ -799,7 +852,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   int64_t nnz_all = 0, gnnz_all = 0;
   for (int h = 0; h < p.Hq; ++h) {
     HostHead& H = P->hh[h];
-    const int64_t* t = ctx->pinned + (size_t)h * NTOT;
+    const int64_t* t = tot + (size_t)h * NTOT;
     H.nnz = t[0];
     H.gnnz = t[1];
     H.nitems = t[2];
@@ -842,7 +895,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
     send(P, pk);
   }
   HIPCHK(launch_work_fill(P->d_heads, p.Hq, d_ib, d_pb, d_sb, max_groups, P->d_items, P->d_splits, st));
-  HIPCHK(hipEventRecord(P->ev[3], st));
+  mark(P, 3, st);
   P->nnz_all = nnz_all;
   P->gnnz_all = gnnz_all;
 }
@@ -867,11 +920,11 @@ static void plan_execute_impl(mmi_plan* P, const void* q, const void* k, const v
   a.part_o = P->d_part_o;
   a.part_ml = P->d_part_ml;
   a.R = P->R;
-  HIPCHK(hipEventRecord(P->ev[4], st));
+  mark(P, 4, st);
   HIPCHK(launch_attention(a, st));
-  HIPCHK(hipEventRecord(P->ev[5], st));
+  mark(P, 5, st);
   HIPCHK(launch_combine(a, P->d_splits, P->nsplit, st));
-  HIPCHK(hipEventRecord(P->ev[6], st));
+  mark(P, 6, st);
   P->stream = st;
   P->executed = true;
 }
@@ -928,6 +981,7 @@ int mmi_ctx_create(int device, mmi_ctx** out) {
     HIPCHK(hipGetDeviceCount(&n));
     if (device < 0 || device >= n) fail(MMI_ERR_INVALID_ARG, "device %d of %d", device, n);
     HIPCHK(hipSetDevice(device));
+    scratch_setup(device);
     auto* c = new mmi_ctx();
     c->device = device;
     if (const char* e = getenv("MMI_CHUNK_BLOCKS")) {
@@ -958,13 +1012,16 @@ int mmi_ctx_destroy(mmi_ctx* ctx) {
   });
 }
 
-int mmi_plan_create(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* cfgs, const void* q,
-                    const void* k, void* stream, mmi_plan** out) {
+// Plan creation shared by mmi_plan_create (scratch_base NULL: buffers from the
+// context's allocator) and mmi_attention_noalloc (buffers in the scratch).
+static int create_plan(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* cfgs, const void* q,
+                       const void* k, void* stream, uint8_t* scratch_base, mmi_plan** out) {
   mmi_plan* P = nullptr;
   int rc = guarded([&] {
     validate_inputs(prob, cfgs, q, k);     // host-only checks first
     if (!ctx || !out) fail(MMI_ERR_INVALID_ARG, "ctx/out is NULL");
     P = new mmi_plan();
+    P->scratch = scratch_base;
     plan_create_impl(ctx, prob, cfgs, q, k, (hipStream_t)stream, P);
   });
   if (rc != MMI_OK) {
@@ -982,6 +1039,11 @@ int mmi_plan_create(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* c
   ++ctx->live_plans;
   *out = P;
   return MMI_OK;
+}
+
+int mmi_plan_create(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* cfgs, const void* q,
+                    const void* k, void* stream, mmi_plan** out) {
+  return create_plan(ctx, prob, cfgs, q, k, stream, nullptr, out);
 }
 
 int mmi_plan_execute(mmi_plan* plan, const void* q, const void* k, const void* v, void* o, float* lse,
@@ -1074,6 +1136,7 @@ int mmi_plan_timing_get(mmi_plan* P, mmi_plan_timing* out) {
     t.computed_blocks = P->nnz_all;
     t.work_items = P->nitems;
     t.loaded_blocks = P->gnnz_all;
+    t.device_bytes = P->device_bytes;
     *out = t;
   });
 }
@@ -1161,6 +1224,26 @@ int mmi_attention(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* cfg
   if (rc != MMI_OK) return rc;
   rc = mmi_plan_execute(P, q, k, v, o, lse, stream);
   const int rc2 = mmi_plan_destroy(P);
+  return rc != MMI_OK ? rc : rc2;
+}
+
+int mmi_attention_noalloc(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg* cfgs, const void* q,
+                          const void* k, const void* v, void* o, float* lse, void* stream) {
+  if (!ctx) {
+    g_last_error = "ctx is NULL";
+    return MMI_ERR_INVALID_ARG;
+  }
+  if (ctx->device >= MAX_DEVICES || !g_scratch_ptr[ctx->device]) {
+    g_last_error = "no-allocation scratch is not set up on this device";
+    return MMI_ERR_UNSUPPORTED;
+  }
+  // one call at a time per device: the scratch holds one plan
+  std::lock_guard<std::mutex> lk(g_scratch_call_mu[ctx->device]);
+  mmi_plan* P = nullptr;
+  int rc = create_plan(ctx, prob, cfgs, q, k, stream, g_scratch_ptr[ctx->device], &P);
+  if (rc != MMI_OK) return rc;
+  rc = mmi_plan_execute(P, q, k, v, o, lse, stream);
+  const int rc2 = mmi_plan_destroy(P);      // waits for the stream: the scratch is free again
   return rc != MMI_OK ? rc : rc2;
 }
 

@@ -66,13 +66,13 @@ class mmi_head_stats(ct.Structure):
 class mmi_plan_timing(ct.Structure):
     _fields_ = [("est_ms", ct.c_float), ("select_ms", ct.c_float), ("index_ms", ct.c_float),
                 ("attn_ms", ct.c_float), ("combine_ms", ct.c_float), ("computed_blocks", ct.c_int64),
-                ("work_items", ct.c_int64), ("loaded_blocks", ct.c_int64)]
+                ("work_items", ct.c_int64), ("loaded_blocks", ct.c_int64), ("device_bytes", ct.c_int64)]
 
 
 SYMBOLS = ["mmi_plan_timing_get", "mmi_version", "mmi_status_str", "mmi_last_error", "mmi_ctx_create", "mmi_ctx_destroy",
            "mmi_plan_create", "mmi_plan_execute", "mmi_plan_stats", "mmi_plan_export",
            "mmi_plan_destroy", "mmi_attention", "mmi_dense_attention", "mmi_permute_rows",
-           "mmi_unpermute_rows", "mmi_output_sqerr"]
+           "mmi_unpermute_rows", "mmi_output_sqerr", "mmi_attention_noalloc"]
 
 _lib = None
 
@@ -97,6 +97,8 @@ def lib():
             "mmi_plan_timing_get": ([vp, ct.POINTER(mmi_plan_timing)], i32),
             "mmi_attention": ([vp, ct.POINTER(mmi_problem), ct.POINTER(mmi_head_cfg), vp, vp, vp, vp, vp,
                                vp], i32),
+            "mmi_attention_noalloc": ([vp, ct.POINTER(mmi_problem), ct.POINTER(mmi_head_cfg), vp, vp, vp, vp,
+                                       vp, vp], i32),
             "mmi_dense_attention": ([vp, ct.POINTER(mmi_problem), vp, vp, vp, vp, vp, vp], i32),
             "mmi_permute_rows": ([vp, i64, vp, i64, vp, i64, i64, vp], i32),
             "mmi_unpermute_rows": ([vp, i64, vp, i64, vp, i64, i64, vp], i32),
@@ -307,6 +309,12 @@ def mmi_attention(ctx, prob, heads, q, k, v, o, lse=None, stream=None):
     cfgs = head_cfgs(heads)
     _check(lib().mmi_attention(ctx.h, ct.byref(prob.c), cfgs, _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
                                _stream(stream)))
+
+
+def mmi_attention_noalloc(ctx, prob, heads, q, k, v, o, lse=None, stream=None):
+    cfgs = head_cfgs(heads)
+    _check(lib().mmi_attention_noalloc(ctx.h, ct.byref(prob.c), cfgs, _ptr(q), _ptr(k), _ptr(v), _ptr(o),
+                                       _ptr(lse), _stream(stream)))
 
 
 def mmi_dense_attention(ctx, prob, q, k, v, o, lse=None, stream=None):

@@ -21,7 +21,7 @@ def declared():
 
 def test_every_declared_symbol_is_exported():
     names = declared()
-    assert len(names) == 16 and set(names) == set(mmi.SYMBOLS)
+    assert len(names) == 17 and set(names) == set(mmi.SYMBOLS)
     L = mmi.lib()
     for n in names:
         assert hasattr(L, n), n
