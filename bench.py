@@ -34,12 +34,12 @@ FLOP_PER_BLOCK = 4 * 64 * 64 * 128
 # HBM traffic of one k_attention launch on the 1M workload, from two rocprofv3
 # --pmc passes (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) scaled by what
 # the same counters read for a plain 1 GiB copy (read x1.939, write x1.000).
-# Keyed by the kernel source's SHA-256 prefix: once the kernel changes the
-# counters are stale and `traffic` is reported as null.
-TRAFFIC = {
-    "abf52cdf35cf5395": {"workload": "cfg4_mm_1m", "fetch_kib": 970954714, "write_kib": 8334266,
-                         "fetch_scale": 1.939, "write_scale": 1.000},
-}
+# Keyed by the SHA-256 prefix of the sources that decide the launch's memory
+# traffic (the kernel, the block index and work list, the runtime that orders
+# them): once any of them changes the counters are stale and `traffic` is
+# reported as null.
+TRAFFIC_SOURCES = ("k_attention.hip", "k_blocks.hip", "runtime.hip")
+TRAFFIC = {}
 
 
 def pattern_head(pattern: str, tpf: int):
@@ -56,12 +56,17 @@ def pattern_head(pattern: str, tpf: int):
             "qb_grid": C.qboundary_head({0: C.ashape(128, 4096), 1: C.grid_window(tpf)})}[pattern]
 
 
-def attention_traffic(workload: str):
+def traffic_key():
     import hashlib
-    src = os.path.join(ROOT, "paper_2504_16083_amd", "csrc", "k_attention.hip")
-    with open(src, "rb") as f:
-        key = hashlib.sha256(f.read()).hexdigest()[:16]
-    t = TRAFFIC.get(key)
+    h = hashlib.sha256()
+    for name in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, "paper_2504_16083_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def attention_traffic(workload: str):
+    t = TRAFFIC.get(traffic_key())
     if t is None or t["workload"] != workload:
         return None
     return (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024.0
@@ -81,12 +86,15 @@ def parse():
                     help="mm: the multi-modal prefill workloads (--config); natten: neighborhood "
                          "attention over a video DiT token grid (Appendix F), bidirectional; search: "
                          "the modality-aware pattern search (Algorithm 4) on its calibration sample")
-    ap.add_argument("--dense-reps", type=int, default=1)
+    ap.add_argument("--dense-reps", type=int, default=3, help="dense baseline runs (median reported)")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--sdpa", action="store_true",
                     help="also time PyTorch's flash SDPA (dense causal) on the same inputs, as context")
-    ap.add_argument("--cpu-rows", type=int, default=8)
+    ap.add_argument("--cpu-blocks", type=int, default=4,
+                    help="query blocks per sampled head whose rows the cpu_baseline oracle computes")
+    ap.add_argument("--no-128k", action="store_true",
+                    help="skip the 128K workload that the default 1M run also reports (metric_128k)")
     ap.add_argument("--pattern", default="method",
                     choices=["method", "ashape", "trishape", "sf_fixed", "sf_strided", "vslash", "grid", "qb_grid"],
                     help="every head on one pattern instead of the workload's per-head patterns: one of "
@@ -99,48 +107,116 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(wl, q, k, v, rows_per_head, heads):
-    """Oracle (numpy fp64) on sampled heads/rows; extrapolated to a full layer."""
+def _scratch_dir():
+    import tempfile
+    for base in ("/dev/shm", tempfile.gettempdir()):
+        try:
+            st = os.statvfs(base)
+            if st.f_bavail * st.f_frsize > (16 << 30):
+                return tempfile.mkdtemp(prefix="mmi_bench_", dir=base)
+        except OSError:
+            continue
+    return tempfile.mkdtemp(prefix="mmi_bench_")
+
+
+def _oracle_head(t):
+    """One head of the cpu_baseline sample, in a worker process (one BLAS
+    thread): the oracle's full plan (estimation, choices, permutations, every
+    block row), then every row of a few uniformly drawn permuted query
+    blocks. Returns the CPU seconds of each part and the selected key blocks
+    of the sampled query blocks and of the whole head."""
     import numpy as np
-    from threadpoolctl import threadpool_info
 
     from oracle import attention as OA
     from oracle import numerics as ON
     from oracle import plan as OP
+    qb = np.load(t["path_q"], mmap_mode="r")[t["qi"]]
+    K = ON.bf16_bits_to_f64(np.asarray(np.load(t["path_k"], mmap_mode="r")[t["kvi"]]))
+    V = ON.bf16_bits_to_f64(np.asarray(np.load(t["path_v"], mmap_mode="r")[t["kvi"]]))
 
+    def q_rows(r):
+        return ON.bf16_bits_to_f64(np.asarray(qb[np.asarray(r, dtype=np.int64)]))
+
+    c0 = time.process_time()
+    hp = OP.plan_head(t["cfg"], t["S"], t["modality"], q_rows, K)
+    c1 = time.process_time()
+    rng = np.random.default_rng(t["seed"])
+    live = [i for i in range(hp.nbq) if (hp.qperm[i * 64:(i + 1) * 64] >= 0).any()]
+    pick = rng.choice(live, size=min(t["blocks"], len(live)), replace=False)
+    rows = np.concatenate([hp.qperm[i * 64:(i + 1) * 64] for i in pick])
+    rows = np.sort(rows[rows >= 0])
+    c2 = time.process_time()
+    OA.head_rows(hp, q_rows, K, V, rows)
+    c3 = time.process_time()
+    return dict(h=t["h"], plan_s=c1 - c0, rows_s=c3 - c2, rows=len(rows),
+                nnz_sample=int(sum(len(hp.blocks[i]) for i in pick)), nnz=int(sum(len(b) for b in hp.blocks)))
+
+
+def cpu_baseline(wl, q, k, v, blocks_per_head, max_workers=16):
+    """The oracle (numpy fp64) on a bounded sample of the layer, timed on this
+    host's cores: one worker process per sampled head (the first `cores`
+    heads, every head kind among them), each running the full oracle plan of
+    its head and every row of `blocks_per_head` random query blocks. Layer
+    CPU time = sum over all heads of (plan time + row time per selected key
+    block x selected key blocks), each head taking the mean of the sampled
+    heads of its configuration; the value is that time spread over the
+    workers (heads and rows are independent)."""
+    import multiprocessing as mp
+    import shutil
+    from concurrent.futures import ProcessPoolExecutor
+
+    import numpy as np
+    import torch
     G = wl.Hq // wl.Hkv
-    t0 = time.perf_counter()
+    n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    cores = max(1, min(max_workers, n, wl.Hq))
+    heads = list(range(cores))
     kvs = sorted({h // G for h in heads})
-    K = {g: ON.torch_bf16_to_f64(k[:, g]) for g in kvs}
-    V = {g: ON.torch_bf16_to_f64(v[:, g]) for g in kvs}
-    t_load = time.perf_counter() - t0
-    rng = np.random.default_rng(0)
-    t_plan, t_rows, n_rows = {}, 0.0, 0
-    for h in heads:
-        qh = q[:, h]
+    t0 = time.perf_counter()
+    tmp = _scratch_dir()
+    try:
+        bits = lambda x: x.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        paths = {nm: os.path.join(tmp, nm + ".npy") for nm in ("q", "k", "v")}
+        np.save(paths["q"], bits(q[:, heads].transpose(0, 1)))
+        np.save(paths["k"], bits(k[:, kvs].transpose(0, 1)))
+        np.save(paths["v"], bits(v[:, kvs].transpose(0, 1)))
+        tasks = [dict(h=h, qi=i, kvi=kvs.index(h // G), cfg=wl.heads[h], S=wl.S, modality=wl.modality,
+                      blocks=blocks_per_head, seed=h, path_q=paths["q"], path_k=paths["k"], path_v=paths["v"])
+                 for i, h in enumerate(heads)]
+        env_old = {x: os.environ.get(x) for x in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")}
+        for x in env_old:
+            os.environ[x] = "1"
+        try:
+            with ProcessPoolExecutor(max_workers=cores, mp_context=mp.get_context("spawn")) as ex:
+                res = list(ex.map(_oracle_head, tasks))
+        finally:
+            for x, val in env_old.items():
+                if val is None:
+                    os.environ.pop(x, None)
+                else:
+                    os.environ[x] = val
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+    wall = time.perf_counter() - t0
 
-        def q_rows(r, qh=qh):
-            import torch
-            return ON.torch_bf16_to_f64(qh[torch.as_tensor(r, device=qh.device)])
-
-        t1 = time.perf_counter()
-        hp = OP.plan_head(wl.heads[h], wl.S, wl.modality, q_rows, K[h // G])
-        t_plan[h] = time.perf_counter() - t1
-        rows = np.sort(rng.choice(wl.S, rows_per_head, replace=False))
-        t2 = time.perf_counter()
-        OA.head_rows(hp, q_rows, K[h // G], V[h // G], rows)
-        t_rows += time.perf_counter() - t2
-        n_rows += len(rows)
-    plan_per_head = sum(t_plan.values()) / len(t_plan)
-    per_row = t_rows / max(n_rows, 1)
-    layer_s = plan_per_head * wl.Hq + per_row * wl.S * wl.Hq
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    return {"value": layer_s * 1e3, "unit": "ms/layer", "cores": threads, "kind": "oracle",
-            "sample": (f"heads {list(heads)}: full oracle plan (estimation, choices, permutations, every "
-                       f"block row) + masked attention of {rows_per_head} random rows per head; "
-                       f"extrapolated as plan_time*Hq + row_time*S*Hq (measured {time.perf_counter() - t0:.1f} s, "
-                       f"incl. {t_load:.1f} s bf16->fp64 load)"),
-            "plan_s_per_head": plan_per_head, "row_ms": per_row * 1e3}
+    def kind(h):
+        c = wl.heads[h]
+        return (c.kind, c.op, tuple(sorted(c.intra.items())), tuple(sorted(c.cross.items())))
+    by_kind = {}
+    for r in res:
+        by_kind.setdefault(kind(r["h"]), []).append(r)
+    layer_s = 0.0
+    for h in range(wl.Hq):
+        rs = by_kind[kind(h)]
+        layer_s += np.mean([r["plan_s"] + r["rows_s"] / max(r["nnz_sample"], 1) * r["nnz"] for r in rs])
+    sample_cpu = sum(r["plan_s"] + r["rows_s"] for r in res)
+    return {"value": layer_s / cores * 1e3, "unit": "ms/layer", "cores": cores, "kind": "oracle",
+            "sample": (f"heads 0-{cores - 1} (every head configuration of the layer), one worker process "
+                       f"each: full oracle plan + all rows of {blocks_per_head} random query blocks "
+                       f"({sum(r['rows'] for r in res)} rows); {sample_cpu:.1f} CPU s in {wall:.1f} s "
+                       f"wall incl. input staging; layer = sum over heads of plan time + row time per "
+                       f"selected key block x selected key blocks, spread over the {cores} cores"),
+            "cpu_s_per_layer": layer_s}
 
 
 def sdpa_context(wl, q, k, v, sparse_ms):
@@ -249,26 +325,17 @@ def main():
     if args.workload == "search":
         search_main(args)
         return
-    import numpy as np
     import torch
 
     from paper_2504_16083_amd import mmi
-    from synth import config as C
-    from synth import generate, workloads
+    from synth import workloads
 
     wl = workloads.natten_video() if args.workload == "natten" else workloads.by_id(args.config)
     if args.pattern != "method":
         wl.heads = [pattern_head(args.pattern, wl.frame or 256)] * wl.Hq
         wl.name = f"{wl.name}+{args.pattern}"
     torch.cuda.set_device(0)
-    log(f"workload {wl.name}: S={wl.S} Hq={wl.Hq} Hkv={wl.Hkv}")
-    q, k, v = generate.make_qkv(wl, "cuda")
-    torch.cuda.synchronize()
-    log("inputs generated")
-    o = torch.empty_like(q)
-    lse = torch.empty(wl.Hq, wl.S, device="cuda", dtype=torch.float32)
     ctx = mmi.Ctx(0)
-    prob = mmi.Problem(wl.S, wl.Hq, wl.Hkv, wl.modality)
     stream = torch.cuda.current_stream()
     if args.calib_copy_mib > 0:
         rows = args.calib_copy_mib * 1024 * 1024 // 256
@@ -279,6 +346,71 @@ def main():
         torch.cuda.synchronize()
         log(f"calibration copy: {rows * 256} bytes read and written")
         del src, dst, ident
+
+    res, q, k, v = measure(wl, args, ctx, stream, sdpa=args.sdpa and args.workload == "mm")
+    cpu = None
+    if not args.no_cpu:
+        log("cpu baseline")
+        cpu = cpu_baseline(wl, q, k, v, args.cpu_blocks)
+        log(f"cpu baseline done: {cpu['sample']}")
+    del q, k, v
+    extra = {}
+    if args.workload == "mm" and args.pattern == "method" and args.config == 4 and not args.no_128k:
+        # the metric's other size: the 128K mixed-modality workload, same steps
+        torch.cuda.empty_cache()
+        r2, *_ = measure(workloads.by_id(2), args, ctx, stream, sdpa=False)
+        extra["metric_128k"] = {"workload": r2["workload"], "ms_per_layer": r2["ms"],
+                                "stages_ms": r2["stages_ms"], "blocks": r2["blocks"],
+                                "roofline": {"achieved": r2["tflops"], "frac": r2["tflops"] / PEAK_BF16_TFLOPS,
+                                             "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"},
+                                "dense": r2["dense"],
+                                "speedup_vs_dense": None if r2["dense"] is None
+                                else r2["dense"]["speedup_sparse_vs_dense"]}
+    out = {
+        "metric": ("neighborhood attention ms/layer (bidirectional, all heads, index + attention)"
+                   if args.workload == "natten" else
+                   "prefill attention ms/layer (sparse, all heads, estimation + index + attention)"),
+        "value": res["ms"], "unit": "ms/layer", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": res["ms"], "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16",
+        "data": ("synthetic (seeded N(0,1) Q/K/V)" if args.workload == "natten"
+                 else "synthetic (seeded Q/K/V with planted grid/text/sink structure)"),
+        "config": {"workload": wl.name, "S": wl.S, "Hq": wl.Hq, "Hkv": wl.Hkv, "head_dim": 128,
+                   "block": 64, "parallelism": "single GPU",
+                   **({k2: wl.extra[k2] for k2 in ("grid", "win", "tile")} if args.workload == "natten" else {})},
+        "stages_ms": res["stages_ms"],
+        "blocks": res["blocks"],
+        "roofline": {"bound": "mfma", "kernel": "k_attention", "achieved": res["tflops"],
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": res["tflops"] / PEAK_BF16_TFLOPS,
+                     "traffic": attention_traffic(wl.name)},
+        "dense": res["dense"],
+        "speedup_vs_dense": None if res["dense"] is None else res["dense"]["speedup_sparse_vs_dense"],
+        **({"sdpa_context": res["sdpa"]} if res["sdpa"] is not None else {}),
+        **extra,
+        "cpu_baseline": cpu,
+        "wall_s": res["wall"],
+    }
+    print(json.dumps(out), flush=True)
+    ctx.close()
+
+
+def measure(wl, args, ctx, stream, sdpa=False):
+    """K timed steps of the whole layer (after W warmup steps) on one
+    workload, with the attention kernel's HIP-event time of each step; then
+    the dense baseline (median of --dense-reps runs) and, if asked, SDPA."""
+    import numpy as np
+    import torch
+
+    from paper_2504_16083_amd import mmi
+    from synth import config as C
+    from synth import generate
+    log(f"workload {wl.name}: S={wl.S} Hq={wl.Hq} Hkv={wl.Hkv}")
+    q, k, v = generate.make_qkv(wl, "cuda")
+    torch.cuda.synchronize()
+    log("inputs generated")
+    o = torch.empty_like(q)
+    lse = torch.empty(wl.Hq, wl.S, device="cuda", dtype=torch.float32)
+    prob = mmi.Problem(wl.S, wl.Hq, wl.Hkv, wl.modality)
 
     def step():
         plan = mmi.Plan(ctx, prob, wl.heads, q, k, stream)
@@ -309,7 +441,8 @@ def main():
     nb = (wl.S + 63) // 64
     causal_blocks = nb * (nb + 1) // 2 * wl.Hq
     dense_heads = [C.global_head(C.dense())] * wl.Hq
-    if args.workload == "natten":
+    natten = wl.heads[0].op.kind == C.OP_NATTEN
+    if natten:
         # bidirectional baseline: the same op with windows as large as the grid
         # allows (odd), which selects every (query tile, key tile) pair
         g, t = wl.extra["grid"], wl.extra["tile"]
@@ -322,67 +455,32 @@ def main():
 
     dense = None
     if not args.no_dense:
-        dense_ms, dense_attn = [], []
+        dense_ms = []
         for _ in range(args.dense_reps):
             plan = mmi.Plan(ctx, prob, dense_heads, q, k, stream)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             plan.execute(q, k, v, o, lse, stream)
             e1.record(stream)
-            t = plan.timing()
             plan.destroy()
             torch.cuda.synchronize()
             dense_ms.append(e0.elapsed_time(e1))
-            dense_attn.append(t["attn_ms"] + t["combine_ms"])
             log(f"dense done: {dense_ms[-1]:.2f} ms")
-        dms = float(min(dense_ms))
-        dense = {"ms_attention": dms, "blocks": causal_blocks,
+        dms = float(np.median(dense_ms))
+        dense = {"ms_attention": dms, "runs_ms": dense_ms, "blocks": causal_blocks,
                  "tflops": causal_blocks * FLOP_PER_BLOCK / (dms * 1e-3) / 1e12,
                  "speedup_sparse_vs_dense": dms / ms}
-
-    sdpa = None
-    if args.sdpa and args.workload == "mm":
-        sdpa = sdpa_context(wl, q, k, v, ms)
-        log(f"sdpa done: {sdpa}")
-
-    cpu = None
-    if not args.no_cpu:
-        kinds, heads = set(), []
-        for h, cfg in enumerate(wl.heads):
-            key = (cfg.kind, cfg.op.kind)
-            if key not in kinds:
-                kinds.add(key)
-                heads.append(h)
-        log(f"cpu baseline on heads {heads}")
-        cpu = cpu_baseline(wl, q, k, v, args.cpu_rows, heads)
-
-    out = {
-        "metric": ("neighborhood attention ms/layer (bidirectional, all heads, index + attention)"
-                   if args.workload == "natten" else
-                   "prefill attention ms/layer (sparse, all heads, estimation + index + attention)"),
-        "value": ms, "unit": "ms/layer", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": ms, "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16",
-        "data": ("synthetic (seeded N(0,1) Q/K/V)" if args.workload == "natten"
-                 else "synthetic (seeded Q/K/V with planted grid/text/sink structure)"),
-        "config": {"workload": wl.name, "S": wl.S, "Hq": wl.Hq, "Hkv": wl.Hkv, "head_dim": 128,
-                   "block": 64, "parallelism": "single GPU",
-                   **({k2: wl.extra[k2] for k2 in ("grid", "win", "tile")} if args.workload == "natten" else {})},
-        "stages_ms": {k2: avg[k2] for k2 in ("est_ms", "select_ms", "index_ms", "attn_ms", "combine_ms")},
-        "blocks": {"computed": blocks, "loaded": loaded,
-                   ("all_pairs" if args.workload == "natten" else "causal"): causal_blocks,
-                   "density": blocks / causal_blocks, "computed_per_load": blocks / max(loaded, 1)},
-        "roofline": {"bound": "mfma", "kernel": "k_attention", "achieved": attn_tflops,
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": attn_tflops / PEAK_BF16_TFLOPS,
-                     "traffic": attention_traffic(wl.name)},
-        "dense": dense,
-        "speedup_vs_dense": None if dense is None else dense["speedup_sparse_vs_dense"],
-        **({"sdpa_context": sdpa} if sdpa is not None else {}),
-        "cpu_baseline": cpu,
-        "wall_s": wall,
-    }
-    print(json.dumps(out), flush=True)
-    ctx.close()
+    sd = None
+    if sdpa:
+        sd = sdpa_context(wl, q, k, v, ms)
+        log(f"sdpa done: {sd}")
+    del o, lse
+    return (dict(workload=wl.name, ms=ms, wall=wall, tflops=attn_tflops, dense=dense, sdpa=sd,
+                 stages_ms={k2: avg[k2] for k2 in ("est_ms", "select_ms", "index_ms", "attn_ms", "combine_ms")},
+                 blocks={"computed": blocks, "loaded": loaded,
+                         ("all_pairs" if natten else "causal"): causal_blocks,
+                         "density": blocks / causal_blocks, "computed_per_load": blocks / max(loaded, 1)}),
+            q, k, v)
 
 
 if __name__ == "__main__":

@@ -26,7 +26,8 @@
  *     h reads KV head h / (Hq / Hkv). Element strides are given per token
  *     and per head; the head dimension must be contiguous and every row
  *     16-byte aligned. Stride 0 means the packed [S, H, 128] layout.
- *     S times the K or V token stride must stay below 2^31 elements.
+ *     S times the K or V token stride must stay below 2^31 elements, and
+ *     the K and V token strides themselves below 2^23 elements.
  *   - The output O must not alias Q, K or V. A plan is not thread-safe.
  */
 #ifndef MMI_H

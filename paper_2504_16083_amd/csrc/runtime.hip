@@ -296,9 +296,12 @@ static mmi_problem normalise(const mmi_problem* pr) {
                          p.v_stride_s, p.v_stride_h, p.o_stride_s, p.o_stride_h};
   for (int i = 0; i < 8; ++i)
     if (st[i] <= 0 || st[i] % 8) fail(MMI_ERR_INVALID_ARG, "strides must be positive multiples of 8 elements");
-  // the attention kernel forms K/V row offsets as 32-bit byte offsets
+  // the attention kernel forms K/V row offsets as 32-bit byte offsets, the
+  // token stride in bytes entering a 24-bit multiply
   if (2 * p.S * p.k_stride_s > (int64_t)UINT32_MAX || 2 * p.S * p.v_stride_s > (int64_t)UINT32_MAX)
     fail(MMI_ERR_UNSUPPORTED, "S x K/V token stride must stay below 2^31 elements");
+  if (2 * p.k_stride_s >= ((int64_t)1 << 24) || 2 * p.v_stride_s >= ((int64_t)1 << 24))
+    fail(MMI_ERR_UNSUPPORTED, "K/V token stride must stay below 2^23 elements");
   if (p.modality) {
     if (p.n_modalities < 1 || p.n_modalities > MMI_MAX_MODALITIES)
       fail(MMI_ERR_INVALID_ARG, "n_modalities must be in [1, %d]", MMI_MAX_MODALITIES);

@@ -80,6 +80,13 @@ def test_validation_codes_without_device():
     mod[3] = 9
     p = mmi.Problem(100, 2, 1, mod); p.c.n_modalities = 2
     assert _create(p, g) == -1
+    # K/V token strides enter a 24-bit multiply in the attention kernel: at
+    # most 2^23 - 8 elements (S = 100 keeps S x stride far below 2^31)
+    for name in ("k", "v"):
+        ok = mmi.Problem(100, 2, 1, strides={name: ((1 << 23) - 8, 128)})
+        assert _create(ok, g) == -1                       # valid up to the ctx
+        bad = mmi.Problem(100, 2, 1, strides={name: (1 << 23, 128)})
+        assert _create(bad, g) == -2 and "2^23" in mmi.mmi_last_error()
 
 
 def test_ctx_without_device_is_an_error():

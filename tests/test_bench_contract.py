@@ -28,3 +28,18 @@ def test_traffic_table_entries_are_well_formed():
         assert t["fetch_kib"] > 0 and t["write_kib"] > 0 and t["fetch_scale"] > 0 and t["write_scale"] > 0
     v = bench.attention_traffic("cfg4_mm_1m")
     assert v is None or v > 0
+
+
+def test_cpu_baseline_sample_and_extrapolation():
+    """The cpu_baseline leg on the 4096-token workload (CPU tensors): one
+    worker per sampled head, every head configuration sampled, a positive
+    extrapolated layer time spread over the workers it used."""
+    sys.path.insert(0, ROOT)
+    import bench
+    from synth import generate, workloads
+    wl = workloads.config0()
+    q, k, v = generate.make_qkv(wl, "cpu")
+    r = bench.cpu_baseline(wl, q, k, v, blocks_per_head=2, max_workers=2)
+    assert r["kind"] == "oracle" and r["unit"] == "ms/layer" and r["cores"] == 2
+    assert r["value"] > 0 and abs(r["value"] - r["cpu_s_per_layer"] / 2 * 1e3) < 1e-6
+    assert "(256 rows)" in r["sample"]          # 2 heads x 2 blocks x 64 rows
