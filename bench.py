@@ -3,7 +3,8 @@
 One step = the whole hot path for one layer (all heads): estimation, choices,
 permutations, block index, block-sparse attention and the output scatter
 (mmi_plan_create + mmi_plan_execute + mmi_plan_destroy through the C-ABI),
-on seeded synthetic inputs already resident in HBM. Prints ONE JSON line.
+on seeded synthetic inputs already resident in HBM, producing the attention
+output O (with --lse also each row's log-sum-exp). Prints ONE JSON line.
 
 Also measured in the same run:
   * dense baseline: every causal block through the same kernel
@@ -93,6 +94,8 @@ def parse():
                     help="also time PyTorch's flash SDPA (dense causal) on the same inputs, as context")
     ap.add_argument("--cpu-blocks", type=int, default=4,
                     help="query blocks per sampled head whose rows the cpu_baseline oracle computes")
+    ap.add_argument("--lse", action="store_true",
+                    help="also ask for each row's log-sum-exp (the prefill layer itself needs only O)")
     ap.add_argument("--no-128k", action="store_true",
                     help="skip the 128K workload that the default 1M run also reports (metric_128k)")
     ap.add_argument("--pattern", default="method",
@@ -376,7 +379,7 @@ def main():
         "data": ("synthetic (seeded N(0,1) Q/K/V)" if args.workload == "natten"
                  else "synthetic (seeded Q/K/V with planted grid/text/sink structure)"),
         "config": {"workload": wl.name, "S": wl.S, "Hq": wl.Hq, "Hkv": wl.Hkv, "head_dim": 128,
-                   "block": 64, "parallelism": "single GPU",
+                   "block": 64, "parallelism": "single GPU", "outputs": "O and LSE" if args.lse else "O",
                    **({k2: wl.extra[k2] for k2 in ("grid", "win", "tile")} if args.workload == "natten" else {})},
         "stages_ms": res["stages_ms"],
         "blocks": res["blocks"],
@@ -409,7 +412,7 @@ def measure(wl, args, ctx, stream, sdpa=False):
     torch.cuda.synchronize()
     log("inputs generated")
     o = torch.empty_like(q)
-    lse = torch.empty(wl.Hq, wl.S, device="cuda", dtype=torch.float32)
+    lse = torch.empty(wl.Hq, wl.S, device="cuda", dtype=torch.float32) if args.lse else None
     prob = mmi.Problem(wl.S, wl.Hq, wl.Hkv, wl.modality)
 
     def step():
@@ -475,7 +478,7 @@ def measure(wl, args, ctx, stream, sdpa=False):
         sd = sdpa_context(wl, q, k, v, ms)
         log(f"sdpa done: {sd}")
     del o, lse
-    return (dict(workload=wl.name, ms=ms, wall=wall, tflops=attn_tflops, dense=dense, sdpa=sd,
+    return (dict(workload=wl.name, lse=bool(args.lse), ms=ms, wall=wall, tflops=attn_tflops, dense=dense, sdpa=sd,
                  stages_ms={k2: avg[k2] for k2 in ("est_ms", "select_ms", "index_ms", "attn_ms", "combine_ms")},
                  blocks={"computed": blocks, "loaded": loaded,
                          ("all_pairs" if natten else "causal"): causal_blocks,

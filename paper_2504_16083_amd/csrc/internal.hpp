@@ -195,7 +195,7 @@ struct AttnArgs {
   const WorkItem* items;
   int64_t nitems;
   float* part_o;              // [nparts][R*64][128], each row normalised by its bf16-P sum
-  float* part_ml;             // [nparts][R*64][2]: running max m and fp32-P sum l
+  float* part_ml;             // [nparts][R*64][4]: running max m, bf16-P sum lo, fp32-P sum l, unused
   int32_t R;                  // query blocks per row group (1, 2 or 4)
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st);

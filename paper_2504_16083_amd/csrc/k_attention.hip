@@ -31,11 +31,13 @@
 // The running maximum is only moved when a row's block maximum exceeds it by
 // more than RESCALE_SLACK (log2 units): P entries then stay below 2^8, which
 // neither bf16 nor the fp32 sums mind, and the O rescale becomes rare.
-// Each row keeps two sums: l over the fp32 P (for the LSE) and lo over the
-// bf16-rounded P that the PV product actually uses (for O = PV / lo). With
-// lo, O is a convex combination of V rows whatever the rounding of P, so a
-// row dominated by one key is not scaled by that key's rounding error (up to
-// 2^-8 relative, which for |V| of several units exceeds the output bound).
+// Each row keeps the sum lo of the bf16-rounded P that the PV product
+// actually uses (O = PV / lo): O is then a convex combination of V rows
+// whatever the rounding of P, so a row dominated by one key is not scaled by
+// that key's rounding error (up to 2^-8 relative, which for |V| of several
+// units exceeds the output bound). Only when the caller asks for the LSE
+// (kernel variant WL) does a row also sum the fp32 P into l, for LSE = m +
+// log l; split rows merge their O by lo in either variant.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -235,6 +237,7 @@ __device__ __forceinline__ float sum8(const bf16x8& p, float acc) {
 // bf16 B operands, row sums into l (fp32 P) and lo (bf16 P). m moves (alpha < 1) only when some row's
 // block maximum passes it by more than RESCALE_SLACK. Branch-free, so that
 // the compiler can interleave it with independent MFMAs.
+template <bool WL>
 __device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m, float& l, float& lo,
                                               bf16x8 (&pb)[4], float& alpha) {
   float mx = NEG_BIG;
@@ -254,7 +257,7 @@ __device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m
     for (int x = 0; x < 16; ++x) {
       const float p = fast_exp2(fmaf(s[kt][x], sc, -m_new));
       s[kt][x] = p;
-      rs += p;
+      if constexpr (WL) rs += p;
     }
   float ro = 0.0f;
 #pragma unroll
@@ -264,7 +267,7 @@ __device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m
     for (int x = 0; x < 8; ++x) pb[stp][x] = (__bf16)s[kt][4 * (2 * half + (x >> 2)) + (x & 3)];
     ro = sum8(pb[stp], ro);
   }
-  l = l * alpha + xhalf_sum(rs);
+  if constexpr (WL) l = l * alpha + xhalf_sum(rs);
   lo = lo * alpha + xhalf_sum(ro);
 }
 
@@ -310,6 +313,7 @@ struct SoftmaxState {
   float mx, m_new, rs, ro;
 };
 
+template <bool WL>
 __device__ __forceinline__ void softmax_piece(int pc, f32x16 (&s)[2], float sc, float& m, float& l, float& lo,
                                               bf16x8 (&pb)[4], float& alpha, SoftmaxState& st) {
   if (pc < 4) {
@@ -330,14 +334,14 @@ __device__ __forceinline__ void softmax_piece(int pc, f32x16 (&s)[2], float sc, 
     const int e = pc - 5, kt = e >> 4, x = e & 15;
     const float p = fast_exp2(fmaf(s[kt][x], sc, -st.m_new));
     s[kt][x] = p;
-    st.rs += p;
+    if constexpr (WL) st.rs += p;
   } else if (pc < 41) {
     const int stp = pc - 37, kt = stp >> 1, half = stp & 1;
 #pragma unroll
     for (int x = 0; x < 8; ++x) pb[stp][x] = (__bf16)s[kt][4 * (2 * half + (x >> 2)) + (x & 3)];
     st.ro = sum8(pb[stp], st.ro);
   } else {
-    l = l * alpha + xhalf_sum(st.rs);
+    if constexpr (WL) l = l * alpha + xhalf_sum(st.rs);
     lo = lo * alpha + xhalf_sum(st.ro);
   }
 }
@@ -347,7 +351,7 @@ __device__ __forceinline__ void softmax_piece(int pc, f32x16 (&s)[2], float sc, 
 // interleaved (MFMA, then a share of the softmax), because the hardware
 // overlaps vector instructions only with MFMAs of the same wave. MFMA A
 // operands are read from LDS three slots ahead.
-template <bool QK, bool PV>
+template <bool QK, bool PV, bool WL>
 __device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, const Stage& vst, f32x16 (&s_qk)[2],
                                            const bf16x8 (&p_cur)[4], f32x16 (&s_sm)[2], bf16x8 (&p_new)[4],
                                            float sc, float& alpha) {
@@ -385,10 +389,10 @@ __device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, cons
     }
     const int pe = (i + 1) * SM_PIECES / (NM > 0 ? NM : 1);
 #pragma unroll
-    for (; pc < pe; ++pc) softmax_piece(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
+    for (; pc < pe; ++pc) softmax_piece<WL>(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
   }
 #pragma unroll
-  for (; pc < SM_PIECES; ++pc) softmax_piece(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
+  for (; pc < SM_PIECES; ++pc) softmax_piece<WL>(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
 }
 
 // Step t. Entries e0..e2 are the union entries t..t+2 (0 past the end): key
@@ -397,7 +401,7 @@ __device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, cons
 // s_sm, `regs` loading block t+3, kpn the key positions of block t+4. The
 // step multiplies P(t)V(t), turns the scores of t+1 into P(t+1) (p_new),
 // computes the scores of t+2 into s_qk, stages t+3 and starts loading t+4.
-template <int R, bool PERM, bool CAUSAL>
+template <int R, bool PERM, bool CAUSAL, bool WL>
 __device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const KeySrc<R>& ks,
                                            BlockRegs<R>& regs, int (&kpn)[Tile<R>::L], int tid, int t, int n,
                                            int e0, int e1, int e2, int e5, f32x16 (&s_qk)[2],
@@ -411,10 +415,10 @@ __device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const KeyS
   float alpha = 1.0f;
   if (a1) {
     if (needs_mask(e1, ws.rb)) mask_block(stg[(t + 1) & (NSTAGE - 1)], mask_limit(ws, CAUSAL), ws.h, s_sm);
-    if (a2 && a0) fused_step<true, true>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
-    else if (a2) fused_step<true, false>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
-    else if (a0) fused_step<false, true>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
-    else fused_step<false, false>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    if (a2 && a0) fused_step<true, true, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    else if (a2) fused_step<true, false, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    else if (a0) fused_step<false, true, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    else fused_step<false, false, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
   } else {
     if (a2) qk_block(kst, ws.qr, ws.c, ws.h, s_qk);
     if (a0) pv_block(vst, p_cur, ws.vlane, ws.o);
@@ -433,7 +437,7 @@ __device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const KeyS
   __syncthreads();
 }
 
-template <int R, bool PERM, bool CAUSAL>
+template <int R, bool PERM, bool CAUSAL, bool WL>
 __device__ __forceinline__ void block_loop(WaveState& ws, Stage* stg, const AttnArgs& a, const HeadDev& hd,
                                            const WorkItem& w, int tid) {
   KeySrc<R> ks;
@@ -469,22 +473,22 @@ __device__ __forceinline__ void block_loop(WaveState& ws, Stage* stg, const Attn
     qk_block(stg[0], ws.qr, ws.c, ws.h, sa);
     if (needs_mask(e0, ws.rb)) mask_block(stg[0], mask_limit(ws, CAUSAL), ws.h, sa);
     float alpha;
-    softmax_block(sa, sc, ws.m, ws.l, ws.lo, pa, alpha);
+    softmax_block<WL>(sa, sc, ws.m, ws.l, ws.lo, pa, alpha);
   }
   if (n > 1 && sel(e1, ws.rb)) qk_block(stg[1], ws.qr, ws.c, ws.h, sb);
   // two steps per trip so that the buffers swap roles without copies
   for (int t = 0; t < n; t += 2) {
     int e5 = es.get(t + 5);
-    block_step<R, PERM, CAUSAL>(ws, stg, ks, regs, kpn, tid, t, n, e0, e1, e2, e5, sa, pa, sb, pb, sc);
+    block_step<R, PERM, CAUSAL, WL>(ws, stg, ks, regs, kpn, tid, t, n, e0, e1, e2, e5, sa, pa, sb, pb, sc);
     e0 = e1; e1 = e2; e2 = e3; e3 = e4; e4 = e5;
     if (t + 1 >= n) break;
     e5 = es.get(t + 6);
-    block_step<R, PERM, CAUSAL>(ws, stg, ks, regs, kpn, tid, t + 1, n, e0, e1, e2, e5, sb, pb, sa, pa, sc);
+    block_step<R, PERM, CAUSAL, WL>(ws, stg, ks, regs, kpn, tid, t + 1, n, e0, e1, e2, e5, sb, pb, sa, pa, sc);
     e0 = e1; e1 = e2; e2 = e3; e3 = e4; e4 = e5;
   }
 }
 
-template <int R>
+template <int R, bool WL>
 __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 ? 2 : 1))) void k_attention(AttnArgs a) {
   __shared__ Stage stg[NSTAGE];
   const int64_t it = item_of_block(blockIdx.x);
@@ -519,14 +523,14 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
   ws.m = NEG_BIG;
   ws.l = 0.0f;
   ws.lo = 0.0f;
-  if (!hd.causal) block_loop<R, true, false>(ws, stg, a, hd, w, tid);
-  else if (hd.kperm) block_loop<R, true, true>(ws, stg, a, hd, w, tid);
-  else block_loop<R, false, true>(ws, stg, a, hd, w, tid);
+  if (!hd.causal) block_loop<R, true, false, WL>(ws, stg, a, hd, w, tid);
+  else if (hd.kperm) block_loop<R, true, true, WL>(ws, stg, a, hd, w, tid);
+  else block_loop<R, false, true, WL>(ws, stg, a, hd, w, tid);
 
   const float m = ws.m, l = ws.l;
   const int qpos = ws.qpos, h = ws.h;
   // every live row has its own key, so lo > 0 unless this part of a split
-  // row selected nothing (then O, l are 0 and the part weighs nothing)
+  // row selected nothing (then O, lo are 0 and the part weighs nothing)
   const float inv = ws.lo > 0.0f ? 1.0f / ws.lo : 0.0f;
   if (w.part < 0) {
     if (qpos >= 0) {
@@ -540,7 +544,7 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
           for (int j = 0; j < 4; ++j) t[j] = (__bf16)(ws.o[dt][4 * i + j] * inv);
           *reinterpret_cast<bf16x4*>(orow + 32 * dt + 8 * i + 4 * h) = t;
         }
-      if (h == 0 && a.lse) a.lse[(int64_t)w.head * a.S + qpos] = (m + fast_log2(l)) * LN2;
+      if (WL && h == 0) a.lse[(int64_t)w.head * a.S + qpos] = (m + fast_log2(l)) * LN2;
     }
   } else {
     const int row = ws.rb * B + half * 32 + ws.c;    // row of the group, 0 .. 64R-1
@@ -554,16 +558,18 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
         *reinterpret_cast<float4*>(po + 32 * dt + 8 * i + 4 * h) = t;
       }
     if (h == 0) {
-      float* ml = a.part_ml + ((int64_t)w.part * (B * R) + row) * 2;
+      float* ml = a.part_ml + ((int64_t)w.part * (B * R) + row) * 4;
       ml[0] = m;
-      ml[1] = l;
+      ml[1] = ws.lo;
+      ml[2] = WL ? l : 0.0f;
     }
   }
 }
 
-// Merge the (O, m, l) partials of a split row group in a fixed order; each
-// partial O_p is already normalised by its own bf16-P sum, and weighs
-// w_p = l_p 2^(m_p - M): M = max m_p, L = sum w_p, O = sum w_p O_p / L.
+// Merge the partials of a split row group in a fixed order; each partial
+// O_p is already normalised by its own bf16-P sum lo_p and weighs
+// w_p = lo_p 2^(m_p - M): M = max m_p, O = sum w_p O_p / sum w_p (the O of
+// the unsplit row), LSE = M + log2 sum l_p 2^(m_p - M) in natural-log units.
 // Workgroup = the 64 rows of query block blockIdx.y of the group, 4 threads per row.
 __global__ __launch_bounds__(256) void k_combine(AttnArgs a, const SplitRow* splits) {
   const SplitRow sr = splits[blockIdx.x];
@@ -576,15 +582,17 @@ __global__ __launch_bounds__(256) void k_combine(AttnArgs a, const SplitRow* spl
   if (qpos < 0) return;
   const int64_t stride = (int64_t)B * a.R;
   float M = NEG_BIG;
-  for (int p = 0; p < sr.nparts; ++p) M = fmaxf(M, a.part_ml[((int64_t)(sr.part0 + p) * stride + row) * 2]);
+  for (int p = 0; p < sr.nparts; ++p) M = fmaxf(M, a.part_ml[((int64_t)(sr.part0 + p) * stride + row) * 4]);
   float acc[32];
 #pragma unroll
   for (int x = 0; x < 32; ++x) acc[x] = 0.0f;
-  float L = 0.0f;
+  float L = 0.0f, Ll = 0.0f;
   for (int p = 0; p < sr.nparts; ++p) {
     const int64_t pr = (int64_t)(sr.part0 + p) * stride + row;
-    const float wgt = a.part_ml[pr * 2 + 1] * fast_exp2(a.part_ml[pr * 2] - M);
+    const float e = fast_exp2(a.part_ml[pr * 4] - M);
+    const float wgt = a.part_ml[pr * 4 + 1] * e;
     L += wgt;
+    Ll += a.part_ml[pr * 4 + 2] * e;
     const float4* src = reinterpret_cast<const float4*>(a.part_o + pr * D + quarter * 32);
 #pragma unroll
     for (int x = 0; x < 8; ++x) {
@@ -602,17 +610,21 @@ __global__ __launch_bounds__(256) void k_combine(AttnArgs a, const SplitRow* spl
     for (int e = 0; e < 8; ++e) t[e] = (__bf16)(acc[8 * x + e] * inv);
     *reinterpret_cast<bf16x8*>(orow + 8 * x) = t;
   }
-  if (quarter == 0 && a.lse) a.lse[(int64_t)sr.head * a.S + qpos] = (M + fast_log2(L)) * LN2;
+  if (quarter == 0 && a.lse) a.lse[(int64_t)sr.head * a.S + qpos] = (M + fast_log2(Ll)) * LN2;
 }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st) {
   if (a.nitems <= 0) return hipSuccess;
   const int64_t run = 8 * XCD_RUN;
   const int64_t grid = (a.nitems + run - 1) / run * run;
-  switch (a.R) {
-    case 1: hipLaunchKernelGGL(k_attention<1>, dim3((unsigned)grid), dim3(128), 0, st, a); break;
-    case 2: hipLaunchKernelGGL(k_attention<2>, dim3((unsigned)grid), dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL(k_attention<4>, dim3((unsigned)grid), dim3(512), 0, st, a); break;
+  const bool wl = a.lse != nullptr;      // the fp32-P row sums only when the LSE is asked for
+  switch (a.R * 2 + (wl ? 1 : 0)) {
+    case 2: hipLaunchKernelGGL((k_attention<1, false>), dim3((unsigned)grid), dim3(128), 0, st, a); break;
+    case 3: hipLaunchKernelGGL((k_attention<1, true>), dim3((unsigned)grid), dim3(128), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((k_attention<2, false>), dim3((unsigned)grid), dim3(256), 0, st, a); break;
+    case 5: hipLaunchKernelGGL((k_attention<2, true>), dim3((unsigned)grid), dim3(256), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((k_attention<4, false>), dim3((unsigned)grid), dim3(512), 0, st, a); break;
+    case 9: hipLaunchKernelGGL((k_attention<4, true>), dim3((unsigned)grid), dim3(512), 0, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -888,7 +888,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   P->d_items = dalloc<WorkItem>(P, P->nitems);
   P->d_splits = dalloc<SplitRow>(P, P->nsplit);
   P->d_part_o = dalloc<float>(P, (size_t)std::max<int64_t>(P->nparts, 1) * B * R * D);
-  P->d_part_ml = dalloc<float>(P, (size_t)std::max<int64_t>(P->nparts, 1) * B * R * 2);
+  P->d_part_ml = dalloc<float>(P, (size_t)std::max<int64_t>(P->nparts, 1) * B * R * 4);
   int64_t *d_ib = nullptr, *d_pb = nullptr, *d_sb = nullptr;
   {
     Pack pk;

@@ -342,3 +342,39 @@ def test_head_counts(ctx, Hq, Hkv):
     heads = [kinds[h % 4] for h in range(Hq)]
     rep = full_check(ctx, S, Hq, Hkv, mod, heads, q, k, v)
     say(f"  nnz={rep.nnz} ties={rep.ties} max|dO|={rep.max_o:.3g}")
+
+
+@pytest.mark.parametrize("chunk", [None, "5"])
+def test_output_without_lse(chunk, monkeypatch):
+    """Without an LSE buffer the kernel skips the fp32 row sums; O (also of
+    split rows, merged by the bf16-P sums) is bitwise the O of the run that
+    writes the LSE, which the oracle tests check."""
+    from paper_2504_16083_amd import mmi
+    say(f"[gpu] O without LSE, chunk {chunk}")
+    if chunk:
+        monkeypatch.setenv("MMI_CHUNK_BLOCKS", chunk)
+    c = mmi.Ctx(0)
+    try:
+        S = 3000
+        mod = _mm_layout(S, 6)
+        q, k, v = _rand_qkv(S, 4, 2, seed=23, scale_k=2.0)
+        heads = [C.global_head(C.dense()), C.global_head(C.grid(20, 40)),
+                 C.qboundary_head({0: C.ashape(32, 200), 1: C.vslash(30, 20)}),
+                 C.boundary2d_head({0: C.ashape(32, 200), 1: C.grid(20, 40)},
+                                   {(0, 1): C.vert(40), (1, 0): C.dense()})]
+        prob = mmi.Problem(S, 4, 2, mod)
+        plan = mmi.Plan(c, prob, heads, q, k)
+        o1, o2 = torch.empty_like(q), torch.empty_like(q)
+        lse = torch.empty(4, S, device="cuda")
+        plan.execute(q, k, v, o1, lse)
+        plan.execute(q, k, v, o2, None)
+        torch.cuda.synchronize()
+        split = sum(plan.stats(h).split_rows for h in range(4))
+        plan.destroy()
+        say(f"  split rows {split}")
+        assert (split > 0) == bool(chunk)
+        assert torch.equal(o1, o2)
+        rep = full_check(c, S, 4, 2, mod, heads, q, k, v)
+        say("  " + rep.line())
+    finally:
+        c.close()
