@@ -66,6 +66,7 @@ class Report:
     global_op: tuple = None                          # (name, op)
     step3: list = field(default_factory=list)        # [Cand] for global, qboundary, 2d
     kind: str = ""
+    own: dict = field(default_factory=dict)          # this search's own picks where others were adopted
 
 
 def _run(cfg, S, mod, Q, K, V):
@@ -109,10 +110,23 @@ def _pick(cands, key, budget):
     return best
 
 
-def search_head(Q, K, V, S: int, modality, cands, xc, target):
+def search_head(Q, K, V, S: int, modality, cands, xc, target, adopt=None):
     """Q, K, V: fp64 [S, D] of one head; cands / xc: [(name, op)] intra and
     cross candidates in table order; target: the FLOPs target op. Returns
-    (HeadCfg, Report)."""
+    (HeadCfg, Report).
+
+    adopt (for comparing another implementation step by step): choices to
+    carry into the later steps instead of this search's own picks, as
+    {("intra", m): name, ("cross", a, b): name, "global": name, "kind":
+    name}; each own pick that differs is kept in Report.own under the same
+    key, and every step is still scored here."""
+    adopt = adopt or {}
+
+    def take(key, own_name):
+        if key in adopt and adopt[key] != own_name:
+            rep.own[key] = own_name
+            return adopt[key]
+        return own_name
     mod = layout.modality_array(S, modality)
     T = layout.positions_of(mod)
     mods = sorted(T)
@@ -129,9 +143,11 @@ def search_head(Q, K, V, S: int, modality, cands, xc, target):
         hp, O = _run(C.boundary2d_head({m: op for m in mods}, none_all), S, mod, Q, K, V)
         cost = _costs_by_modality(hp)
         rep.step1.append(Cand(name, cost, {m: _sqerr(O, ref1, T[m]) for m in mods}))
+    ops1 = dict(cands, target=target)
     for m in mods:
         c = _pick(rep.step1, m, rep.budget1[m])
-        rep.intra[m] = (c.name, dict(cands)[c.name]) if c else ("target", target)
+        name = take(("intra", m), c.name if c else "target")
+        rep.intra[m] = (name, ops1[name])
     intra = {m: rep.intra[m][1] for m in mods}
 
     # step 2: cross-modality search
@@ -151,7 +167,8 @@ def search_head(Q, K, V, S: int, modality, cands, xc, target):
         for ai, a in enumerate(mods):
             b = mods[(ai + k) % n]
             c = _pick(rep.step2[k], a, rep.budget1[a] - intra_cost[a])
-            rep.cross[(a, b)] = (c.name, dict(xc)[c.name]) if c else ("none", C.none())
+            name = take(("cross", a, b), c.name if c else "none")
+            rep.cross[(a, b)] = (name, dict(xc, none=C.none())[name])
     cross = {ab: v[1] for ab, v in rep.cross.items()}
 
     # step 3: inter-modality search
@@ -163,7 +180,8 @@ def search_head(Q, K, V, S: int, modality, cands, xc, target):
         rep.step3_global.append(Cand(name, {"all": sum(len(b) for b in hp.blocks)},
                                      {"all": _sqerr(O, ref, allrows)}))
     c = _pick(rep.step3_global, "all", rep.budget3)
-    rep.global_op = (c.name, dict(cands)[c.name]) if c else ("target", target)
+    name = take("global", c.name if c else "target")
+    rep.global_op = (name, ops1[name])
     heads = [("global", C.global_head(rep.global_op[1])), ("qboundary", C.qboundary_head(intra)),
              ("2d", C.boundary2d_head(intra, cross))]
     for name, cfg in heads:
@@ -172,5 +190,5 @@ def search_head(Q, K, V, S: int, modality, cands, xc, target):
     c = _pick(rep.step3, "all", rep.budget3)
     if c is None:
         c = min(rep.step3, key=lambda x: x.cost["all"])
-    rep.kind = c.name
-    return dict(heads)[c.name], rep
+    rep.kind = take("kind", c.name)
+    return dict(heads)[rep.kind], rep

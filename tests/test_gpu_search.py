@@ -1,8 +1,9 @@
 """GPU pattern search (Algorithm 4 through libmmi) against the oracle's, on
 the 4096-token text/video sample with the scaled search space of the oracle
-pins: every candidate's block cost bit-exact, errors within the bf16 output
-band, the same choices (a different one only where the oracle's errors of
-the two are inside that band)."""
+pins: every candidate's block cost bit-exact and errors within the bf16
+output band at all three steps (the oracle carries the GPU's choices
+forward), and the same choices (a different one only where the oracle's
+errors of the two are inside that band)."""
 import math
 
 import numpy as np
@@ -12,7 +13,7 @@ import torch
 from oracle import search as OS
 from synth import config as C
 
-from parity import say
+from parity import full_check, say
 from test_oracle_search import S, F, sample, small_space
 
 pytestmark = pytest.mark.gpu
@@ -36,6 +37,10 @@ def _same_choice(got, want, scored, key, rows):
 
 
 def test_search_matches_oracle():
+    """All three steps compared, whatever was chosen before: the oracle
+    carries the GPU's choices into its later steps (adopt) and keeps its own
+    picks beside them; every own pick that differs must be a tie inside the
+    bf16 error band. Costs bit-exact, errors in the band, at every step."""
     from paper_2504_16083_amd import mmi
     from paper_2504_16083_amd import search as GS
     mod, (Q, K, V) = sample()
@@ -49,33 +54,46 @@ def test_search_matches_oracle():
         ctx.close()
     say(f"[gpu] search: {nplans} plans; kinds {[r.kind for r in reps]}")
     rows = {m: int((mod == m).sum()) for m in (0, 1)}
+    ties = 0
     for h in range(2):
-        cfg, orep = OS.search_head(Q[:, h], K[:, 0], V[:, 0], S, mod, cands, xc, target)
         g = reps[h]
+        adopt = {("intra", m): g.intra[m][0] for m in (0, 1)}
+        adopt.update({("cross",) + ab: g.cross[ab][0] for ab in g.cross})
+        adopt.update({"global": g.global_op[0], "kind": g.kind})
+        cfg, orep = OS.search_head(Q[:, h], K[:, 0], V[:, 0], S, mod, cands, xc, target, adopt=adopt)
         say(f"  head {h}: gpu {g.kind} {[g.intra[m][0] for m in (0, 1)]} {[v2[0] for v2 in g.cross.values()]} "
-            f"{g.global_op[0]}; oracle {orep.kind} {[orep.intra[m][0] for m in (0, 1)]} "
-            f"{[v2[0] for v2 in orep.cross.values()]} {orep.global_op[0]}")
+            f"{g.global_op[0]}; oracle's own differing picks {orep.own}")
         assert g.budget1 == orep.budget1 and g.budget3 == orep.budget3
         for a, b in zip(g.step1, orep.step1):
             assert a.name == b.name and a.cost == b.cost, (a, b)
             for m in (0, 1):
                 assert _close(a.err[m], b.err[m], rows[m]), (h, a.name, m, a.err[m], b.err[m])
-        for m in (0, 1):
-            assert _same_choice(g.intra[m][0], orep.intra[m][0], orep.step1, m, rows[m])
-        for a, b in zip(g.step2[1], orep.step2[1]):
-            assert a.name == b.name and a.cost == b.cost, (a, b)
-            for m in (0, 1):
-                assert _close(a.err[m], b.err[m], rows[m])
-        for ab in orep.cross:
-            assert _same_choice(g.cross[ab][0], orep.cross[ab][0], orep.step2[1], ab[0], rows[ab[0]])
+        for kk in g.step2:
+            assert [a.name for a in g.step2[kk]] == [b.name for b in orep.step2[kk]]
+            for a, b in zip(g.step2[kk], orep.step2[kk]):
+                assert a.cost == b.cost, (a, b)
+                for m in (0, 1):
+                    assert _close(a.err[m], b.err[m], rows[m])
         for a, b in zip(g.step3_global, orep.step3_global):
             assert a.name == b.name and a.cost == b.cost
             assert _close(a.err["all"], b.err["all"], S)
-        if g.intra == orep.intra and g.cross == orep.cross and g.global_op == orep.global_op:
-            for a, b in zip(g.step3, orep.step3):
-                assert a.name == b.name and a.cost == b.cost
-                assert _close(a.err["all"], b.err["all"], S)
-            assert _same_choice(g.kind, orep.kind, orep.step3, "all", S)
+        for a, b in zip(g.step3, orep.step3):
+            assert a.name == b.name and a.cost == b.cost
+            assert _close(a.err["all"], b.err["all"], S)
+        # a pick of the oracle's own that differs from the GPU's is a tie
+        for key, own in orep.own.items():
+            ties += 1
+            if key[0] == "intra":
+                assert _same_choice(g.intra[key[1]][0], own, orep.step1, key[1], rows[key[1]]), key
+            elif key[0] == "cross":
+                a, b = key[1:]
+                kk = (b - a) % 2                 # the step-2 round that decides pair (a, b)
+                assert _same_choice(g.cross[(a, b)][0], own, orep.step2[kk], a, rows[a]), key
+            elif key == "global":
+                assert _same_choice(g.global_op[0], own, orep.step3_global, "all", S), key
+            else:
+                assert _same_choice(g.kind, own, orep.step3, "all", S), key
+    say(f"  ties {ties}")
 
 
 def test_search_calibration_costs():
@@ -115,8 +133,23 @@ def test_search_calibration_costs():
         assert sc.name == name
         got, want = sc.cost, costs(op)
         if got != want:
-            # only an estimated choice (Grid stride/phase, VS lines) on a near-tie may differ
-            assert op.kind in (C.OP_GRID, C.OP_VSLASH), (name, got, want)
-            mism.append(name)
+            mism.append((name, op, got, want))
             say(f"  {name}: cost {got} vs oracle {want}")
-    assert len(mism) <= 2, mism
+    # a different cost is accepted only as the consequence of a tied choice:
+    # the candidate's plan for head 0 passes the layered comparison (which
+    # accepts a different Grid stride/phase or VS selection only inside the
+    # tie band, then checks the block index under the GPU's choice) with at
+    # least one tie
+    none_all = {(0, 1): C.none(), (1, 0): C.none()}
+    for name, op, got, want in mism:
+        cfg = C.boundary2d_head({0: op, 1: op}, none_all)
+        rows = np.arange(wl.S - 256, wl.S)
+        ctx = mmi.Ctx(0)
+        try:
+            rep = full_check(ctx, wl.S, wl.Hq, wl.Hkv, wl.modality, [cfg] * wl.Hq, q, k, v, rows=rows,
+                             heads_to_check=[0])
+        finally:
+            ctx.close()
+        say(f"  {name}: " + rep.line())
+        assert rep.ties, (name, got, want)
+        assert sum(rep.nnz.values()) == sum(got.values())

@@ -109,3 +109,35 @@ def test_one_modality_reduces_to_the_global_search():
     for c in rep.step1:
         assert c.cost[0] == g[c.name].cost["all"]
         assert abs(c.err[0] - g[c.name].err["all"]) <= 1e-9 * max(1.0, c.err[0])
+
+
+def test_adopted_choices_are_carried_into_later_steps(searched):
+    """Adopting the search's own picks changes nothing; adopting another
+    intra choice records the own pick, scores step 1 the same, and builds
+    the step-2 candidates on the adopted intra ops (so their costs and
+    errors are those of a search whose step 1 chose it)."""
+    mod, (Q, K, V), cfg, rep = searched
+    cands, xc, target = small_space()
+    own = {("intra", m): rep.intra[m][0] for m in (0, 1)}
+    own.update({("cross",) + ab: rep.cross[ab][0] for ab in rep.cross})
+    own.update({"global": rep.global_op[0], "kind": rep.kind})
+    cfg2, rep2 = OS.search_head(Q[:, 0], K[:, 0], V[:, 0], S, mod, cands, xc, target, adopt=own)
+    assert rep2.own == {} and rep2.kind == rep.kind and rep2.intra == rep.intra and rep2.cross == rep.cross
+    other = next(n for n, _ in cands if n != rep.intra[1][0] and n.startswith("ashape"))
+    cfg3, rep3 = OS.search_head(Q[:, 0], K[:, 0], V[:, 0], S, mod, cands, xc, target,
+                                adopt={("intra", 1): other})
+    assert rep3.own == {("intra", 1): rep.intra[1][0]} and rep3.intra[1][0] == other
+    assert [(c.name, c.cost, c.err) for c in rep3.step1] == [(c.name, c.cost, c.err) for c in rep.step1]
+    # step 2 ran with the adopted video op: its candidates' costs equal a
+    # direct plan of that configuration
+    intra = {0: rep.intra[0][1], 1: dict(cands)[other]}
+    cross = {(0, 1): C.dense(), (1, 0): C.dense()}
+    name, op = xc[1]
+    cross[(0, 1)] = op
+    hp = P.plan_head(C.boundary2d_head(intra, cross), S, mod, lambda r: Q[r, 0], K[:, 0])
+    off, arr = hp.groups[1]
+    lo, hi = off // 64, off // 64 + (len(arr) + 63) // 64
+    want = sum(int(((bs >= lo) & (bs < hi)).sum()) for i, bs in enumerate(hp.blocks)
+               if P._group_of_block(hp, i)[0] == 0)
+    got = next(c for c in rep3.step2[1] if c.name == name).cost[0]
+    assert got == want
