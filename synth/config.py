@@ -87,45 +87,19 @@ def trishape(sink: int, local: int, bottom: int) -> Op:
     return Op(OP_TRISHAPE, sink=sink, local=local, bottom=bottom)
 
 
-def natten(grid, win, tile=None) -> Op:
+def natten(grid, win, tile) -> Op:
     """Neighborhood attention over a (T, H, W) token grid (T = 1 for images),
     bidirectional: each token sees the win_t x win_h x win_w neighborhood
     around it, shifted inside the grid at the borders. Tokens are permuted
-    tile by tile (tile_t x tile_h x tile_w = 64 tokens = one block); the
-    default tile is the one with the fewest selected blocks."""
+    tile by tile (tile_t x tile_h x tile_w = 64 tokens = one block); the tile
+    shape is the caller's choice."""
     grid, win = tuple(int(x) for x in grid), tuple(int(x) for x in win)
-    if tile is None:
-        tile = natten_best_tile(grid, win)
     return Op(OP_NATTEN, grid=grid, win=win, tile=tuple(int(x) for x in tile))
 
 
 def natten_tiles():
     """Tile shapes (powers of two, 64 tokens)."""
     return [(1 << a, 1 << b, 1 << (6 - a - b)) for a in range(7) for b in range(7 - a)]
-
-
-def natten_best_tile(grid, win):
-    """Tile with the fewest selected (query tile, key tile) pairs: per axis the
-    key-tile span of every query tile, multiplied over the axes (smallest
-    padding on ties). Host-side choice of an input parameter; the block sets
-    themselves come from the library and the oracle."""
-    best = None
-    for tile in natten_tiles():
-        pairs, slots = 1, 1
-        for n, k, t in zip(grid, win, tile):
-            nt = -(-n // t)
-            span = 0
-            for a in range(nt):
-                c0, c1 = a * t, min(n, a * t + t) - 1
-                lo = min(max(c0 - k // 2, 0), n - k)
-                hi = min(max(c1 - k // 2, 0), n - k) + k - 1
-                span += hi // t - lo // t + 1
-            pairs *= span
-            slots *= nt * t
-        key = (pairs, slots)
-        if best is None or key < best[0]:
-            best = (key, tile)
-    return best[1]
 
 
 def vert(n: int) -> Op:

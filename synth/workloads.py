@@ -156,11 +156,12 @@ def natten_video() -> Workload:
     a 33 x 45 x 80 token grid (118,800 tokens: the latent of a 129-frame
     720p clip under 4x temporal / 8x spatial compression and 2 x 2 patches),
     24 heads without GQA, 9 x 15 x 15 windows (about 1.7% of the tokens per
-    query), tile chosen by fewest selected blocks. Plain N(0, 1) Q/K/V: the
+    query), tiles of 2 x 4 x 8 tokens (the power-of-two tile with the fewest
+    selected tile pairs for these windows). Plain N(0, 1) Q/K/V: the
     pattern is static, nothing is estimated from the data."""
     grid, win, H = (33, 45, 80), (9, 15, 15), 24
     S = grid[0] * grid[1] * grid[2]
-    op = C.natten(grid, win)
+    op = C.natten(grid, win, (2, 4, 8))
     st = Structure(sigma=[1] * H, amp=0.0)
     return Workload("natten_video_119k", S, H, H, np.zeros(S, np.uint8), [C.global_head(op)] * H, st,
                     SEED0 + 5, extra={"grid": grid, "win": win, "tile": op.tile})

@@ -55,7 +55,8 @@ def random_head(rng, S, mods):
     if k == 1:
         g = factor3(rng, S)
         win = tuple(int(rng.integers(0, (n + 1) // 2)) * 2 + 1 for n in g)
-        return C.global_head(C.natten(g, win))
+        tiles = C.natten_tiles()
+        return C.global_head(C.natten(g, win, tiles[(7 * g[0] + 3 * g[1] + g[2]) % len(tiles)]))
     if k == 2:
         return C.qboundary_head({m: random_op(rng) for m in mods})
     cross = {}

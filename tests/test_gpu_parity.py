@@ -147,7 +147,7 @@ def test_natten(ctx):
     q, k, v = _rand_qkv(S, 5, 1, seed=19)
     heads = [
         C.global_head(C.natten((6, 20, 24), (3, 7, 9), (2, 4, 8))),
-        C.global_head(C.natten((1, 48, 60), (1, 11, 11))),
+        C.global_head(C.natten((1, 48, 60), (1, 11, 11), (1, 8, 8))),
         C.global_head(C.natten((6, 20, 24), (5, 19, 23), (1, 8, 8))),
         C.global_head(C.natten((5, 24, 24), (3, 5, 7), (4, 4, 4))),
         C.global_head(C.natten((3, 30, 32), (1, 1, 1), (1, 4, 16))),

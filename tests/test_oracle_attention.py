@@ -86,3 +86,27 @@ def test_planted_grid_recovered_end_to_end():
         hp = P.plan_head(wl.heads[h], wl.S, wl.modality, lambda r: Q[r, h], K[:, 0])
         st = hp.ops["g"]
         assert (st.sigma, st.p) == (252, planted_phase)
+
+
+def test_planted_jittered_strides_recovered():
+    """The 32K workload plants one stride per KV group (255 + U{-4..4}) and
+    searches strides within 8 of 255: one Grid head of every KV group must
+    find its group's stride, and the phase of its vertical line (128 text
+    tokens come first)."""
+    wl = workloads.config1()
+    q, k, _ = generate.make_qkv(wl, "cpu")
+    G = wl.Hq // wl.Hkv
+    firsts = {}
+    for h, c in enumerate(wl.heads):
+        if c.op.kind == C.OP_GRID:
+            firsts.setdefault(h // G, h)
+    assert sorted(firsts) == list(range(wl.Hkv))
+    assert len(set(wl.structure.sigma)) > 1                   # the strides do differ
+    for g, h in firsts.items():
+        sig = wl.structure.sigma[g]
+        K = numerics.torch_bf16_to_f64(k[:, g])
+        qh = q[:, h]
+        hp = P.plan_head(wl.heads[h], wl.S, wl.modality,
+                         lambda r: numerics.torch_bf16_to_f64(qh[torch.as_tensor(r)]), K)
+        st = hp.ops["g"]
+        assert (st.sigma, st.p) == (sig, (128 + wl.structure.line_slot[g]) % sig), (g, h)

@@ -95,7 +95,3 @@ def test_bidirectional_attention_matches_torch():
     O2, L2 = A.permuted_blockwise(hp, Q, K, V)
     assert np.abs(O2 - ref).max() < 1e-12 and np.abs(L2 - L).max() < 1e-12
 
-
-def test_tile_choice_prefers_square_tiles_for_square_windows():
-    assert C.natten_best_tile((1, 64, 64), (1, 13, 13)) == (1, 8, 8)
-    assert C.natten_best_tile((16, 32, 32), (7, 7, 7)) == (4, 4, 4)
