@@ -153,10 +153,12 @@ hipError_t launch_perms(const HeadDev* heads, int nheads, const OpDev* ops, Grou
 hipError_t launch_qb_order(const QbOrderJob* jobs, int njobs, const uint8_t* modpos, int S, hipStream_t st);
 int qb_order_chunks(int S);
 // k_estimate.hip
-hipError_t launch_est_lse(const RowSet* rs, int nrs, int max_chunks, Tensor q, Tensor k,
-                          int chunk_keys, hipStream_t st);
-hipError_t launch_est_scores(const EstJob* jobs, int njobs, int max_tiles, const RowSet* rs,
-                             Tensor q, Tensor k, hipStream_t st);
+// order: [ngrp][nr] member indices (-1 = none) of the groups that read the
+// same keys (row sets of one KV head; jobs of one KV head and key map).
+hipError_t launch_est_lse(const RowSet* rs, int nrs, const int32_t* order, int ngrp, int nr, int max_chunks,
+                          Tensor q, Tensor k, int chunk_keys, hipStream_t st);
+hipError_t launch_est_scores(const EstJob* jobs, int njobs, const int32_t* order, int ngrp, int nr, int max_tiles,
+                             const RowSet* rs, Tensor q, Tensor k, hipStream_t st);
 hipError_t launch_est_udiag(const EstJob* jobs, int njobs, int max_L, hipStream_t st);
 // k_select.hip
 hipError_t launch_grid_search(const GridJob* jobs, int njobs, int max_cands, hipStream_t st);

@@ -16,6 +16,11 @@
 // K rows are read straight from HBM into MFMA operands (each lane loads one
 // contiguous 128-byte half row; the next tile's rows load while the current
 // one is reduced); no LDS staging is needed for S^T = K Q^T.
+// Scheduling: the query sets that read the same keys (one KV head; for the
+// score pass also one key coordinate system) form a group. The workgroups of
+// all members of a group over one key range are consecutive in a run that
+// goes to one XCD, so the range comes from HBM once and from that XCD's L2
+// for the other members.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -24,6 +29,14 @@ namespace mmi {
 namespace {
 
 constexpr float SC = 0.08838834764831845f * LOG2E;   // sqrt(1/128) * log2(e)
+
+// Logical work index of physical workgroup b when runs of `run` consecutive
+// logical items go to one XCD (workgroups are dispatched to the 8 XCDs in
+// turn) and the runs to XCDs in turn.
+__device__ __forceinline__ int64_t run_item(int64_t b, int run) {
+  const int64_t xcd = b & 7, k = b >> 3;
+  return (k / run) * (8 * (int64_t)run) + xcd * run + (k % run);
+}
 
 __device__ __forceinline__ void load_q_operand(bf16x8 (&qr)[8], const Tensor& q, int head, int pos,
                                                int h) {
@@ -54,9 +67,17 @@ __device__ __forceinline__ f32x16 key_product(const bf16x8 (&ka)[8], const bf16x
 
 }  // namespace
 
-__global__ __launch_bounds__(128) void k_est_lse(const RowSet* sets, Tensor q, Tensor k, int chunk_keys) {
-  const RowSet rs = sets[blockIdx.x];
-  const int ch = blockIdx.y;
+// Logical item = (group, key chunk, member): order[group * nr + member] is a
+// row-set index (-1 = none), nch chunks per group.
+__global__ __launch_bounds__(128) void k_est_lse(const RowSet* sets, const int32_t* order, int ngrp, int nr,
+                                                 int nch, Tensor q, Tensor k, int chunk_keys) {
+  const int64_t lg = run_item(blockIdx.x, nr);
+  const int64_t pair = lg / nr;
+  const int grp = (int)(pair / nch), ch = (int)(pair % nch);
+  if (grp >= ngrp) return;
+  const int si = order[grp * nr + (int)(lg % nr)];
+  if (si < 0) return;
+  const RowSet rs = sets[si];
   if (ch >= rs.nchunks) return;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
   const int r = wave * 32 + c;
@@ -123,12 +144,20 @@ constexpr int EST_TPW = 8;    // 64-key tiles per workgroup of the score pass
 // are loaded once, and the next tile's key positions and K rows load while
 // the current tile is reduced. The arithmetic of every tile is the same as
 // one tile per workgroup.
-__global__ __launch_bounds__(128) void k_est_scores(const EstJob* jobs, const RowSet* sets, Tensor q,
-                                                    Tensor k) {
+// Logical item = (group, run of EST_TPW tiles, member): order[group * nr +
+// member] is a job index (-1 = none), nrun runs per group.
+__global__ __launch_bounds__(128) void k_est_scores(const EstJob* jobs, const int32_t* order, int ngrp, int nr,
+                                                    int nrun, const RowSet* sets, Tensor q, Tensor k) {
   __shared__ float ahat[B * APITCH];
   __shared__ int kposl[B];      // key positions of the current tile, INT_BIG past L_c
-  const EstJob jb = jobs[blockIdx.x];
-  const int ta = blockIdx.y * EST_TPW;
+  const int64_t lg = run_item(blockIdx.x, nr);
+  const int64_t pair = lg / nr;
+  const int grp = (int)(pair / nrun), tr = (int)(pair % nrun);
+  if (grp >= ngrp) return;
+  const int ji = order[grp * nr + (int)(lg % nr)];
+  if (ji < 0) return;
+  const EstJob jb = jobs[ji];
+  const int ta = tr * EST_TPW;
   if (ta >= jb.ntiles) return;
   const int tb = min(ta + EST_TPW, jb.ntiles);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
@@ -217,19 +246,28 @@ __global__ __launch_bounds__(256) void k_est_udiag(const EstJob* jobs) {
   jb.u[o] = acc;
 }
 
-hipError_t launch_est_lse(const RowSet* rs, int nrs, int max_chunks, Tensor q, Tensor k, int chunk_keys,
-                          hipStream_t st) {
+// Workgroups for ngrp groups x nper items x nr members, rounded up to whole
+// runs of nr on each of the 8 XCDs.
+static unsigned grouped_grid(int ngrp, int nper, int nr) {
+  const int64_t items = (int64_t)ngrp * nper * nr, run = 8 * (int64_t)nr;
+  return (unsigned)((items + run - 1) / run * run);
+}
+
+hipError_t launch_est_lse(const RowSet* rs, int nrs, const int32_t* order, int ngrp, int nr, int max_chunks,
+                          Tensor q, Tensor k, int chunk_keys, hipStream_t st) {
   if (nrs <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_est_lse, dim3(nrs, max_chunks), dim3(128), 0, st, rs, q, k, chunk_keys);
+  hipLaunchKernelGGL(k_est_lse, dim3(grouped_grid(ngrp, max_chunks, nr)), dim3(128), 0, st, rs, order, ngrp, nr,
+                     max_chunks, q, k, chunk_keys);
   hipLaunchKernelGGL(k_est_merge, dim3(nrs), dim3(64), 0, st, rs);
   return hipGetLastError();
 }
 
-hipError_t launch_est_scores(const EstJob* jobs, int njobs, int max_tiles, const RowSet* rs, Tensor q,
-                             Tensor k, hipStream_t st) {
+hipError_t launch_est_scores(const EstJob* jobs, int njobs, const int32_t* order, int ngrp, int nr, int max_tiles,
+                             const RowSet* rs, Tensor q, Tensor k, hipStream_t st) {
   if (njobs <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_est_scores, dim3(njobs, (max_tiles + EST_TPW - 1) / EST_TPW), dim3(128), 0, st, jobs, rs,
-                     q, k);
+  const int nrun = (max_tiles + EST_TPW - 1) / EST_TPW;
+  hipLaunchKernelGGL(k_est_scores, dim3(grouped_grid(ngrp, nrun, nr)), dim3(128), 0, st, jobs, order, ngrp, nr,
+                     nrun, rs, q, k);
   return hipGetLastError();
 }
 

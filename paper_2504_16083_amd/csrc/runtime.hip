@@ -786,6 +786,28 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   const Tensor tq{q, p.q_stride_s, p.q_stride_h}, tk{k, p.k_stride_s, p.k_stride_h};
   if (!P->scratch)
     for (auto& e : P->ev) HIPCHK(hipEventCreate(&e));
+  // members of the estimation groups that read the same keys: row sets per
+  // KV head, score jobs per (KV head, key map)
+  auto grouped = [](int n, auto key_of, int& ngrp, int& nr) {
+    std::map<std::pair<int64_t, int64_t>, std::vector<int32_t>> by;
+    for (int i = 0; i < n; ++i) by[key_of(i)].push_back(i);
+    ngrp = (int)by.size();
+    nr = 1;
+    for (const auto& kv : by) nr = std::max(nr, (int)kv.second.size());
+    std::vector<int32_t> order((size_t)std::max(ngrp, 1) * nr, -1);
+    int gi = 0;
+    for (const auto& kv : by) {
+      std::copy(kv.second.begin(), kv.second.end(), order.begin() + (size_t)gi * nr);
+      ++gi;
+    }
+    return order;
+  };
+  int rs_ngrp = 0, rs_nr = 1, job_ngrp = 0, job_nr = 1;
+  const std::vector<int32_t> rs_order = grouped((int)bd.rowsets.size(), [&](int i) {
+    return std::make_pair((int64_t)bd.rowsets[i].kvh, (int64_t)0); }, rs_ngrp, rs_nr);
+  const std::vector<int32_t> job_order = grouped((int)bd.jobs.size(), [&](int i) {
+    return std::make_pair((int64_t)bd.jobs[i].kvh, (int64_t)(intptr_t)bd.jobs[i].keymap); }, job_ngrp, job_nr);
+  int32_t *d_rs_order = nullptr, *d_job_order = nullptr;
   RowSet* d_rs = nullptr;
   EstJob* d_jobs = nullptr;
   GridJob* d_g = nullptr;
@@ -800,11 +822,15 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
     pk.add(P->heads, P->d_heads);
     pk.add(P->ops, P->d_ops);
     pk.add(qjobs, d_qj);
+    pk.add(rs_order, d_rs_order);
+    pk.add(job_order, d_job_order);
     send(P, pk);
   }
   mark(P, 0, st);
-  HIPCHK(launch_est_lse(d_rs, (int)bd.rowsets.size(), bd.max_chunks, tq, tk, bd.chunk_keys, st));
-  HIPCHK(launch_est_scores(d_jobs, (int)bd.jobs.size(), bd.max_tiles, d_rs, tq, tk, st));
+  HIPCHK(launch_est_lse(d_rs, (int)bd.rowsets.size(), d_rs_order, rs_ngrp, rs_nr, bd.max_chunks, tq, tk,
+                        bd.chunk_keys, st));
+  HIPCHK(launch_est_scores(d_jobs, (int)bd.jobs.size(), d_job_order, job_ngrp, job_nr, bd.max_tiles, d_rs, tq,
+                           tk, st));
   HIPCHK(launch_est_udiag(d_jobs, (int)bd.jobs.size(), bd.max_L, st));
   mark(P, 1, st);
   HIPCHK(launch_grid_search(d_g, (int)bd.gjobs.size(), bd.max_cands, st));
