@@ -184,6 +184,10 @@ hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int min_chunk, i
                               int64_t* totals, hipStream_t st);
 hipError_t launch_blocks_fill(const HeadDev* heads, int nheads, int max_nbq, int R, int max_groups,
                               hipStream_t st);
+// Modelled cost of each work item (its union entries: one staged K/V block
+// each, plus one computed block per member that selects it).
+hipError_t launch_item_cost(const HeadDev* heads, const WorkItem* items, int64_t nitems, float* cost,
+                            hipStream_t st);
 hipError_t launch_work_fill(const HeadDev* heads, int nheads, const int64_t* item_base,
                             const int64_t* part_base, const int64_t* split_base, int max_groups,
                             WorkItem* items, SplitRow* splits, hipStream_t st);
@@ -196,6 +200,8 @@ struct AttnArgs {
   const HeadDev* heads;
   const WorkItem* items;
   int64_t nitems;
+  const int32_t* item_map;    // [8][map_len]: work items of each XCD in order, -1 = none
+  int64_t map_len;
   float* part_o;              // [nparts][R*64][128], each row normalised by its bf16-P sum
   float* part_ml;             // [nparts][R*64][4]: running max m, bf16-P sum lo, fp32-P sum l, unused
   int32_t R;                  // query blocks per row group (1, 2 or 4)

@@ -170,14 +170,13 @@ struct EntryStream {
 };
 
 // Work-item order: hardware hands consecutive workgroups to the 8 XCDs in
-// turn. Runs of XCD_RUN consecutive items go to one XCD, and the runs are
-// interleaved across XCDs, so neighbouring row groups (which share key
-// blocks) meet in one L2 while heavy and light heads stay spread out.
-constexpr int XCD_RUN = 32;
-
-__device__ __forceinline__ int64_t item_of_block(int64_t b) {
-  const int64_t xcd = b & 7, k = b >> 3;
-  return (k / XCD_RUN) * (8 * XCD_RUN) + xcd * XCD_RUN + (k % XCD_RUN);
+// turn, so workgroup b runs on XCD b mod 8 as that XCD's (b / 8)-th. The
+// plan's item map lists each XCD's items in order (runs of neighbouring row
+// groups, which share key blocks in that XCD's L2, balanced over the XCDs by
+// modelled cost).
+__device__ __forceinline__ int64_t item_of_block(const AttnArgs& a, int64_t b) {
+  const int64_t k = b >> 3;
+  return k < a.map_len ? a.item_map[(b & 7) * a.map_len + k] : -1;
 }
 
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
@@ -491,8 +490,8 @@ __device__ __forceinline__ void block_loop(WaveState& ws, Stage* stg, const Attn
 template <int R, bool WL>
 __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 ? 2 : 1))) void k_attention(AttnArgs a) {
   __shared__ Stage stg[NSTAGE];
-  const int64_t it = item_of_block(blockIdx.x);
-  if (it >= a.nitems) return;
+  const int64_t it = item_of_block(a, blockIdx.x);
+  if (it < 0 || it >= a.nitems) return;
   const WorkItem w = a.items[it];
   const HeadDev hd = a.heads[w.head];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -615,8 +614,7 @@ __global__ __launch_bounds__(256) void k_combine(AttnArgs a, const SplitRow* spl
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t st) {
   if (a.nitems <= 0) return hipSuccess;
-  const int64_t run = 8 * XCD_RUN;
-  const int64_t grid = (a.nitems + run - 1) / run * run;
+  const int64_t grid = 8 * a.map_len;
   const bool wl = a.lse != nullptr;      // the fp32-P row sums only when the LSE is asked for
   switch (a.R * 2 + (wl ? 1 : 0)) {
     case 2: hipLaunchKernelGGL((k_attention<1, false>), dim3((unsigned)grid), dim3(128), 0, st, a); break;

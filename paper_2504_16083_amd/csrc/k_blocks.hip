@@ -656,6 +656,36 @@ __global__ __launch_bounds__(256) void k_work_fill(const HeadDev* heads, const i
   }
 }
 
+// Cost weights: a staged K/V block costs about 1.5 computed blocks (the
+// attention kernel's time fitted over the 1M workloads: 2.6 ms per million
+// staged blocks, 1.75 ms per million computed blocks).
+constexpr float COST_STAGE = 1.5f, COST_COMPUTE = 1.0f;
+
+// One wave per item: sum over its union entries of the staged block and the
+// computed blocks (select flags, bits 16-23).
+__global__ __launch_bounds__(256) void k_item_cost(const HeadDev* heads, const WorkItem* items, int64_t nitems,
+                                                   float* cost) {
+  const int64_t it = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (it >= nitems) return;
+  const int lane = threadIdx.x & 63;
+  const WorkItem w = items[it];
+  const int32_t* g = heads[w.head].gcol;
+  float acc = 0.0f;
+  for (int e = w.e0 + lane; e < w.e1; e += 64)
+    acc += COST_STAGE + COST_COMPUTE * (float)__popc(((uint32_t)g[e] >> 16) & 0xffu);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) cost[it] = acc;
+}
+
+hipError_t launch_item_cost(const HeadDev* heads, const WorkItem* items, int64_t nitems, float* cost,
+                            hipStream_t st) {
+  if (nitems <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_item_cost, dim3((unsigned)((nitems + 3) / 4)), dim3(256), 0, st, heads, items, nitems,
+                     cost);
+  return hipGetLastError();
+}
+
 hipError_t launch_work_fill(const HeadDev* heads, int nheads, const int64_t* item_base,
                             const int64_t* part_base, const int64_t* split_base, int max_groups,
                             WorkItem* items, SplitRow* splits, hipStream_t st) {

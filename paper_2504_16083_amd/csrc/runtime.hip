@@ -126,6 +126,8 @@ struct mmi_ctx {
   int device = 0;
   int chunk_blocks = 64;           // smallest work-item length (union entries)
   int items_per_layer = 8192;      // target number of work items per layer
+  int split_above_avg = 6;         // with enough row groups, split only groups above this many times
+                                   // their head's average union (0: always split to the item target)
   int row_group = 4;               // query blocks per attention work item (1, 2 or 4)
   int live_plans = 0;              // plans created from this context and not destroyed
   mmi::Allocator alloc;
@@ -182,6 +184,8 @@ struct mmi_plan {
   float* d_part_o = nullptr;
   float* d_part_ml = nullptr;
   int64_t nitems = 0, nsplit = 0, nparts = 0;
+  int32_t* d_item_map = nullptr;  // [8][map_len] work items per XCD
+  int64_t map_len = 0;
   int R = 1;                      // query blocks per attention work item
   int32_t* d_tpos = nullptr;
   std::vector<uint8_t> mod;       // host modality of every position (all 0 without a layout)
@@ -530,6 +534,8 @@ static void validate_inputs(const mmi_problem* prob, const mmi_head_cfg* cfgs, c
   validate_cfgs(L.g, p, cfgs);
 }
 
+static void build_item_map(mmi_plan* P, hipStream_t st);
+
 static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi_head_cfg* cfgs, const void* q,
                              const void* k, hipStream_t st, mmi_plan* P) {
   const mmi_problem p = normalise(prob_in);
@@ -856,7 +862,7 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   // in place of neighbouring groups, which do).
   int64_t groups_all = 0;
   for (const auto& hd : P->heads) groups_all += (hd.nbq + R - 1) / R;
-  const int split_above_avg = groups_all >= ctx->items_per_layer ? 6 : 0;
+  const int split_above_avg = groups_all >= ctx->items_per_layer ? ctx->split_above_avg : 0;
   HIPCHK(launch_blocks_scan(P->d_heads, p.Hq, chunk, items_per_head, split_above_avg, d_tot, st));
   std::vector<int64_t> tot_host;
   const int64_t* tot = nullptr;
@@ -924,9 +930,59 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
     send(P, pk);
   }
   HIPCHK(launch_work_fill(P->d_heads, p.Hq, d_ib, d_pb, d_sb, max_groups, P->d_items, P->d_splits, st));
+  build_item_map(P, st);
   mark(P, 3, st);
   P->nnz_all = nnz_all;
   P->gnnz_all = gnnz_all;
+}
+
+// Work items of each XCD. Items (row groups, or chunks of long ones, in head
+// and group order) are cut into runs of consecutive items, which share key
+// blocks; the runs are dealt to the 8 XCDs longest first, each to the XCD
+// with the least modelled cost so far (at most a quarter more runs than the
+// average per XCD), and each XCD runs its runs in that order. Runs are 32
+// items, fewer for small layers so that every XCD gets some.
+static void build_item_map(mmi_plan* P, hipStream_t st) {
+  const int64_t n = P->nitems;
+  if (n <= 0) return;
+  float* d_cost = dalloc<float>(P, n);
+  HIPCHK(launch_item_cost(P->d_heads, P->d_items, n, d_cost, st));
+  std::vector<float> cost(n);
+  HIPCHK(hipMemcpyAsync(cost.data(), d_cost, sizeof(float) * n, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipStreamSynchronize(st));
+  const int64_t run = std::max<int64_t>(1, std::min<int64_t>(32, n / 64));
+  const int64_t nruns = (n + run - 1) / run;
+  std::vector<double> rc(nruns, 0.0);
+  for (int64_t i = 0; i < n; ++i) rc[i / run] += cost[i];
+  std::vector<int64_t> order(nruns);
+  for (int64_t j = 0; j < nruns; ++j) order[j] = j;
+  std::stable_sort(order.begin(), order.end(), [&](int64_t x, int64_t y) { return rc[x] > rc[y]; });
+  const int64_t avg = (nruns + 7) / 8, cap = avg + std::max<int64_t>(1, avg / 4);
+  double load[8] = {0};
+  std::vector<int64_t> runs_of[8];
+  for (int64_t j : order) {
+    int best = -1;
+    for (int x = 0; x < 8; ++x)
+      if ((int64_t)runs_of[x].size() < cap && (best < 0 || load[x] < load[best])) best = x;
+    runs_of[best].push_back(j);
+    load[best] += rc[j];
+  }
+  int64_t len = 0;
+  std::vector<int64_t> items_of(8, 0);
+  for (int x = 0; x < 8; ++x) {
+    for (int64_t j : runs_of[x]) items_of[x] += std::min(run, n - j * run);
+    len = std::max(len, items_of[x]);
+  }
+  std::vector<int32_t> map((size_t)8 * len, -1);
+  for (int x = 0; x < 8; ++x) {
+    int64_t k = 0;
+    for (int64_t j : runs_of[x])
+      for (int64_t i = j * run; i < std::min(n, (j + 1) * run); ++i) map[(size_t)x * len + k++] = (int32_t)i;
+  }
+  Pack pk;
+  pk.add(map, P->d_item_map);
+  send(P, pk);
+  P->map_len = len;
 }
 
 static void plan_execute_impl(mmi_plan* P, const void* q, const void* k, const void* v, void* o, float* lse,
@@ -948,6 +1004,8 @@ static void plan_execute_impl(mmi_plan* P, const void* q, const void* k, const v
   a.nitems = P->nitems;
   a.part_o = P->d_part_o;
   a.part_ml = P->d_part_ml;
+  a.item_map = P->d_item_map;
+  a.map_len = P->map_len;
   a.R = P->R;
   mark(P, 4, st);
   HIPCHK(launch_attention(a, st));
@@ -1020,6 +1078,10 @@ int mmi_ctx_create(int device, mmi_ctx** out) {
     if (const char* e = getenv("MMI_ITEMS_PER_LAYER")) {
       const int v = atoi(e);
       if (v >= 1) c->items_per_layer = v;
+    }
+    if (const char* e = getenv("MMI_SPLIT_ABOVE_AVG")) {
+      const int v = atoi(e);
+      if (v >= 0) c->split_above_avg = v;
     }
     if (const char* e = getenv("MMI_ROW_GROUP")) {
       const int v = atoi(e);
