@@ -13,14 +13,16 @@
 //   scores are bitwise reproducible.
 // The query rows are contiguous positions [row0, row0+nrows), nrows <= 64,
 // and contiguous in the key coordinate system too (coordinate coord0 + r).
-// K rows are read straight from HBM into MFMA operands (each lane loads one
-// contiguous 128-byte half row; the next tile's rows load while the current
-// one is reduced); no LDS staging is needed for S^T = K Q^T.
-// Scheduling: the query sets that read the same keys (one KV head; for the
-// score pass also one key coordinate system) form a group. The workgroups of
-// all members of a group over one key range are consecutive in a run that
-// goes to one XCD, so the range comes from HBM once and from that XCD's L2
-// for the other members.
+// The query sets that read the same keys (pass 1: one KV head; pass 2 also
+// one key coordinate system) form a group, and the work of a group over one
+// key range runs back to back on one XCD. Pass 1 takes up to four sets of a
+// group per workgroup (two waves each, 32 rows per wave, the query rows in
+// registers as the MFMA B operand): each 64-key tile is loaded once by all
+// 512 threads into LDS (the next tile's rows load while the current one is
+// multiplied) and read as the A operand by every set. Pass 2 takes one job
+// per workgroup and reads its K rows straight from HBM into MFMA operands
+// (the next tile's rows load while the current one is reduced); the jobs of
+// a group over one range find it in that XCD's L2.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -29,6 +31,8 @@ namespace mmi {
 namespace {
 
 constexpr float SC = 0.08838834764831845f * LOG2E;   // sqrt(1/128) * log2(e)
+constexpr int EKP = 136;          // bf16 per staged K row (272 B: conflict-free operand reads)
+constexpr int EMEM = 4;           // query sets (LSE pass) or score jobs per workgroup, 2 waves each
 
 // Logical work index of physical workgroup b when runs of `run` consecutive
 // logical items go to one XCD (workgroups are dispatched to the 8 XCDs in
@@ -38,6 +42,10 @@ __device__ __forceinline__ int64_t run_item(int64_t b, int run) {
   return (k / run) * (8 * (int64_t)run) + xcd * run + (k % run);
 }
 
+struct __align__(16) EstStage {
+  uint16_t k[B * EKP];
+};
+
 __device__ __forceinline__ void load_q_operand(bf16x8 (&qr)[8], const Tensor& q, int head, int pos,
                                                int h) {
   const uint16_t* row = reinterpret_cast<const uint16_t*>(q.p) + (int64_t)head * q.sh +
@@ -45,6 +53,35 @@ __device__ __forceinline__ void load_q_operand(bf16x8 (&qr)[8], const Tensor& q,
 #pragma unroll
   for (int s = 0; s < 8; ++s) qr[s] = pos >= 0 ? load16(row + 8 * s) : zero8();
 }
+
+// This thread's 32 bytes of key row kpos (zeros for kpos < 0): thread
+// (key, part) of the 512 stages dims [16 part, 16 part + 16) of one key.
+__device__ __forceinline__ void fetch_key(bf16x8 (&r)[2], const Tensor& k, int kvh, int kpos, int part) {
+  const uint16_t* row = reinterpret_cast<const uint16_t*>(k.p) + (int64_t)kvh * k.sh +
+                        (int64_t)max(kpos, 0) * k.ss + part * 16;
+  r[0] = kpos >= 0 ? load16(row) : zero8();
+  r[1] = kpos >= 0 ? load16(row + 8) : zero8();
+}
+
+__device__ __forceinline__ void stage_key(EstStage& st, const bf16x8 (&r)[2], int key, int part) {
+  *reinterpret_cast<bf16x8*>(&st.k[key * EKP + part * 16]) = r[0];
+  *reinterpret_cast<bf16x8*>(&st.k[key * EKP + part * 16 + 8]) = r[1];
+}
+
+// S^T of the 64 staged keys x this wave's 32 queries: s[kt] holds keys
+// 32 kt + 8i + 4h + j for query c in element 4i + j.
+__device__ __forceinline__ void staged_product(const EstStage& st, const bf16x8 (&qr)[8], int c, int h,
+                                               f32x16 (&s)[2]) {
+  const f32x16 zero = {};
+#pragma unroll
+  for (int st8 = 0; st8 < 8; ++st8) {
+    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&st.k[c * EKP + h * 64 + st8 * 8]);
+    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&st.k[(32 + c) * EKP + h * 64 + st8 * 8]);
+    s[0] = mfma32(k0, qr[st8], st8 == 0 ? zero : s[0]);
+    s[1] = mfma32(k1, qr[st8], st8 == 0 ? zero : s[1]);
+  }
+}
+
 
 // This lane's half of key row kpos (zeros for kpos < 0): the K operand of
 // one 32-key S^T tile.
@@ -67,56 +104,90 @@ __device__ __forceinline__ f32x16 key_product(const bf16x8 (&ka)[8], const bf16x
 
 }  // namespace
 
-// Logical item = (group, key chunk, member): order[group * nr + member] is a
-// row-set index (-1 = none), nch chunks per group.
-__global__ __launch_bounds__(128) void k_est_lse(const RowSet* sets, const int32_t* order, int ngrp, int nr,
-                                                 int nch, Tensor q, Tensor k, int chunk_keys) {
-  const int64_t lg = run_item(blockIdx.x, nr);
-  const int64_t pair = lg / nr;
+// Pass 1. Logical item = (group, key chunk, batch of EMEM members):
+// order[group * nr + member] is a row-set index (-1 = none); the row sets
+// of a group share one KV head, so every 64-key tile of the chunk is staged
+// once in LDS and multiplied by all members' query rows. Waves w and w + 4
+// hold rows 0-31 and 32-63 of member w. Per row: running (max, sum) of
+// 2^(tau log2e q.k) over its causal keys of the chunk, the fixed order of
+// the tiles, then the two key halves of each tile.
+__global__ __launch_bounds__(512) void k_est_lse(const RowSet* sets, const int32_t* order, int ngrp, int nr,
+                                                 int nbat, int nch, Tensor q, Tensor k, int chunk_keys) {
+  __shared__ EstStage stg[2];
+  const int64_t lg = run_item(blockIdx.x, nbat);
+  const int bat = (int)(lg % nbat);
+  const int64_t pair = lg / nbat;
   const int grp = (int)(pair / nch), ch = (int)(pair % nch);
   if (grp >= ngrp) return;
-  const int si = order[grp * nr + (int)(lg % nr)];
-  if (si < 0) return;
-  const RowSet rs = sets[si];
-  if (ch >= rs.nchunks) return;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
-  const int r = wave * 32 + c;
-  const int qpos = r < rs.nrows ? rs.row0 + r : -1;
+  int kend = 0;                        // keys [0, kend) are visible to some member
+  for (int m = 0; m < EMEM; ++m) {
+    const int mi = bat * EMEM + m;
+    const int si = mi < nr ? order[grp * nr + mi] : -1;
+    if (si >= 0) kend = max(kend, sets[si].row0 + sets[si].nrows);
+  }
+  const int k0 = ch * chunk_keys;
+  if (k0 >= kend) return;
+  const int k1 = min(k0 + chunk_keys, kend);
+  const int kvh = sets[order[grp * nr]].kvh;
+  const int mem = wave & (EMEM - 1), half = wave >> 2;
+  const int mi = bat * EMEM + mem;
+  const int si = mi < nr ? order[grp * nr + mi] : -1;
+  RowSet rs{};
+  if (si >= 0) rs = sets[si];
+  const bool active = si >= 0 && ch < rs.nchunks;
+  const int r = half * 32 + c;
+  const int qpos = active && r < rs.nrows ? rs.row0 + r : -1;
   bf16x8 qr[8];
   load_q_operand(qr, q, rs.head, qpos, h);
-  const int limit = rs.row0 + rs.nrows;           // keys [0, limit) can be visible
-  const int k0 = ch * chunk_keys;
-  const int k1 = min(k0 + chunk_keys, limit);
+  const int key = tid >> 3, part = tid & 7;
+  const int ntile = (k1 - k0 + B - 1) / B;
+  bf16x8 rg[2];
+  fetch_key(rg, k, kvh, k0 + key < k1 ? k0 + key : -1, part);
+  stage_key(stg[0], rg, key, part);
+  if (ntile > 1) fetch_key(rg, k, kvh, k0 + B + key < k1 ? k0 + B + key : -1, part);
+  __syncthreads();
   float m = NEG_BIG, l = 0.0f;
-  bf16x8 ka[8];
-  load_key(ka, k, rs.kvh, k0 + c < k1 ? k0 + c : -1, h);
-  for (int kb = k0; kb < k1; kb += 32) {
-    const f32x16 s = key_product(ka, qr);
-    // the next tile's keys load while this one is reduced
-    if (kb + 32 < k1) load_key(ka, k, rs.kvh, kb + 32 + c < k1 ? kb + 32 + c : -1, h);
-    float mx = NEG_BIG;
-    float x[16];
+  for (int t = 0; t < ntile; ++t) {
+    const int kb = k0 + t * B;
+    if (active) {
+      f32x16 s[2];
+      staged_product(stg[t & 1], qr, c, h, s);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int kt = 0; kt < 2; ++kt) {
+        float mx = NEG_BIG;
+        float x[16];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int key = kb + 8 * i + 4 * h + j;
-        const float v = s[4 * i + j] * SC;
-        x[4 * i + j] = (key < k1 && key <= qpos) ? v : -INFINITY;
-        mx = fmaxf(mx, x[4 * i + j]);
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int kk = kb + kt * 32 + 8 * i + 4 * h + j;
+            const float v = s[kt][4 * i + j] * SC;
+            x[4 * i + j] = (kk < k1 && kk <= qpos) ? v : -INFINITY;
+            mx = fmaxf(mx, x[4 * i + j]);
+          }
+        const float mn = fmaxf(m, mx);
+        float acc = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc += fast_exp2(x[e] - mn);
+        l = l * fast_exp2(m - mn) + acc;
+        m = mn;
       }
-    const float mn = fmaxf(m, mx);
-    float acc = 0.0f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) acc += fast_exp2(x[e] - mn);
-    l = l * fast_exp2(m - mn) + acc;
-    m = mn;
+    }
+    // tile t+1 was loaded during tile t-1; its stage was last read in tile t-1
+    if (t + 1 < ntile) {
+      stage_key(stg[(t + 1) & 1], rg, key, part);
+      const int nk = k0 + (t + 2) * B + key;
+      if (t + 2 < ntile) fetch_key(rg, k, kvh, nk < k1 ? nk : -1, part);
+    }
+    __syncthreads();
   }
+  if (!active) return;
   const float m2 = __shfl_xor(m, 32), l2 = __shfl_xor(l, 32);
   const float mt = fmaxf(m, m2);
   const float lt = h == 0 ? l * fast_exp2(m - mt) + l2 * fast_exp2(m2 - mt)
                           : l2 * fast_exp2(m2 - mt) + l * fast_exp2(m - mt);
-  if (h == 0) {
+  if (h == 0 && r < rs.nrows) {
     float* p = rs.part + ((int64_t)ch * LASTQ + r) * 2;
     p[0] = mt;
     p[1] = lt;
@@ -256,8 +327,9 @@ static unsigned grouped_grid(int ngrp, int nper, int nr) {
 hipError_t launch_est_lse(const RowSet* rs, int nrs, const int32_t* order, int ngrp, int nr, int max_chunks,
                           Tensor q, Tensor k, int chunk_keys, hipStream_t st) {
   if (nrs <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_est_lse, dim3(grouped_grid(ngrp, max_chunks, nr)), dim3(128), 0, st, rs, order, ngrp, nr,
-                     max_chunks, q, k, chunk_keys);
+  const int nbat = (nr + EMEM - 1) / EMEM;
+  hipLaunchKernelGGL(k_est_lse, dim3(grouped_grid(ngrp, max_chunks, nbat)), dim3(512), 0, st, rs, order, ngrp, nr,
+                     nbat, max_chunks, q, k, chunk_keys);
   hipLaunchKernelGGL(k_est_merge, dim3(nrs), dim3(64), 0, st, rs);
   return hipGetLastError();
 }
