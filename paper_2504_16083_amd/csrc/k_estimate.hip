@@ -21,8 +21,9 @@
 // 512 threads into LDS (the next tile's rows load while the current one is
 // multiplied) and read as the A operand by every set. Pass 2 takes one job
 // per workgroup and reads its K rows straight from HBM into MFMA operands
-// (the next tile's rows load while the current one is reduced); the jobs of
-// a group over one range find it in that XCD's L2.
+// (two tiles of rows in registers: tile t + 2 loads while t and t + 1 are
+// multiplied and reduced); the jobs of a group over one range find it in
+// that XCD's L2.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -212,12 +213,12 @@ constexpr int APITCH = 65;
 constexpr int EST_TPW = 8;    // 64-key tiles per workgroup of the score pass
 
 // Each workgroup takes EST_TPW consecutive tiles of one job: the query rows
-// are loaded once, and the next tile's key positions and K rows load while
-// the current tile is reduced. The arithmetic of every tile is the same as
+// are loaded once, and the key positions and K rows of the tile after next
+// load while the current tile is reduced. The arithmetic of every tile is the same as
 // one tile per workgroup.
 // Logical item = (group, run of EST_TPW tiles, member): order[group * nr +
 // member] is a job index (-1 = none), nrun runs per group.
-__global__ __launch_bounds__(128) void k_est_scores(const EstJob* jobs, const int32_t* order, int ngrp, int nr,
+__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void k_est_scores(const EstJob* jobs, const int32_t* order, int ngrp, int nr,
                                                     int nrun, const RowSet* sets, Tensor q, Tensor k) {
   __shared__ float ahat[B * APITCH];
   __shared__ int kposl[B];      // key positions of the current tile, INT_BIG past L_c
@@ -238,28 +239,25 @@ __global__ __launch_bounds__(128) void k_est_scores(const EstJob* jobs, const in
   bf16x8 qr[8];
   load_q_operand(qr, q, jb.head, qpos, h);
   auto key_pos = [&](int kap) { return kap < jb.L_c ? (jb.keymap ? jb.keymap[kap] : kap) : -1; };
-  int kp[2];
-  bf16x8 ka[2][8];
+  // two tiles of K rows in registers: tile t + 2 loads while tiles t and t + 1 are used
+  int kp[2][2];
+  bf16x8 ka[2][2][8];
+  auto fetch = [&](int buf, int t) {
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt) {
-    kp[kt] = key_pos(ta * B + kt * 32 + c);
-    load_key(ka[kt], k, jb.kvh, kp[kt], h);
-  }
-  for (int t = ta; t < tb; ++t) {
+    for (int kt = 0; kt < 2; ++kt) {
+      kp[buf][kt] = key_pos(t * B + kt * 32 + c);
+      load_key(ka[buf][kt], k, jb.kvh, kp[buf][kt], h);
+    }
+  };
+  auto tile = [&](int buf, int t) {
     f32x16 s[2];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) s[kt] = key_product(ka[kt], qr);
+    for (int kt = 0; kt < 2; ++kt) s[kt] = key_product(ka[buf][kt], qr);
     if (wave == 0 && h == 0) {
-      kposl[c] = kp[0] >= 0 ? kp[0] : INT_BIG;
-      kposl[32 + c] = kp[1] >= 0 ? kp[1] : INT_BIG;
+      kposl[c] = kp[buf][0] >= 0 ? kp[buf][0] : INT_BIG;
+      kposl[32 + c] = kp[buf][1] >= 0 ? kp[buf][1] : INT_BIG;
     }
-    if (t + 1 < tb) {
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        kp[kt] = key_pos((t + 1) * B + kt * 32 + c);
-        load_key(ka[kt], k, jb.kvh, kp[kt], h);
-      }
-    }
+    if (t + 2 < tb) fetch(buf, t + 2);
     __syncthreads();
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
@@ -292,6 +290,12 @@ __global__ __launch_bounds__(128) void k_est_scores(const EstJob* jobs, const in
       jb.dpart[(int64_t)t * 128 + d] = acc;
     }
     __syncthreads();    // ahat and kposl are rewritten by the next tile
+  };
+  fetch(0, ta);
+  if (ta + 1 < tb) fetch(1, ta + 1);
+  for (int t = ta; t < tb; t += 2) {
+    tile(0, t);
+    if (t + 1 < tb) tile(1, t + 1);
   }
 }
 
