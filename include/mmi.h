@@ -293,6 +293,73 @@ int mmi_unpermute_rows(const void* src, int64_t src_stride, void* dst, int64_t d
 int mmi_output_sqerr(const mmi_problem* prob, const void* a, const void* b, const uint8_t* cls,
                      int32_t n_class, double* out, void* stream);
 
+/* ------------------------------------------------------------ debug checks
+ * Host-side consistency checks of a plan's tables: when they pass, every
+ * index the attention kernel derives from the tables (permutation slots,
+ * key blocks, union entries, work items, partial slots, the per-XCD item
+ * map) lies inside its buffers. With MMI_DEBUG=1 in the environment when a
+ * context is created, every plan creation of that context runs
+ * mmi_plan_check before it returns, and every execute synchronises with its
+ * stream and reports a failed launch itself. A violation returns
+ * MMI_ERR_INTERNAL; mmi_last_error names the table, head, index and value.
+ * Plain host code: the two view checks need no device. */
+
+/* One head's block index, as mmi_plan_export returns it (host arrays). */
+typedef struct mmi_index_view {
+  int32_t S;
+  int32_t n_qblocks, n_kblocks;  /* mmi_head_stats */
+  int32_t n_layouts;             /* key layouts kperm holds one after another (Q-Boundary heads with
+                                    Grid modalities: more than 1), each n_kblocks / n_layouts blocks */
+  int32_t causal;                /* 0: bidirectional head (mask bits mark padding only) */
+  const int32_t* qperm;          /* [n_qblocks*64] slot -> position or -1, NULL = identity */
+  const int32_t* kperm;          /* [n_kblocks*64], NULL = identity */
+  const int32_t* row_ptr;        /* [n_qblocks+1] */
+  const int32_t* col_idx;        /* [row_ptr[n_qblocks]] */
+  int32_t group_size;            /* query blocks per row group (1, 2 or 4) */
+  int32_t group_stride;          /* mmi_head_stats.group_stride */
+  int32_t n_groups;              /* 0: the row-group checks are skipped */
+  const int32_t* union_ptr;      /* [n_groups+1] (MMI_EXPORT_UNION_PTR) */
+  const int32_t* union_ent;      /* [union_ptr[n_groups]] (MMI_EXPORT_UNION) */
+} mmi_index_view;
+
+/* Checks: qperm and each kperm layout hold every position of [0, S)
+ * exactly once (other slots -1); row_ptr starts at 0 and never decreases,
+ * column indices lie in [0, n_kblocks) and ascend within a row; per row
+ * group (member r = query block (g / rho) R rho + g % rho + r rho): union_ptr
+ * starts at 0 and never decreases, each entry names a key block once, its
+ * select bits name live members only, the blocks of every live member come
+ * first, each part ascending, member r's select bits mark exactly its query
+ * block's column indices, and its mask bit is set exactly where the block
+ * holds a key position above the member's smallest query position (or
+ * padding; a bidirectional head: padding only). */
+int mmi_check_index(const mmi_index_view* v);
+
+/* The attention work list of a plan (host arrays). */
+typedef struct mmi_work_view {
+  int32_t n_heads;
+  const int32_t* n_groups;             /* [n_heads] row groups per head */
+  const int32_t* const* union_ptr;     /* [n_heads] -> [n_groups[h]+1] */
+  int64_t n_items;
+  const int32_t* items;                /* [n_items][5]: head, group, first and end union entry, partial
+                                          slot (-1: the item writes O itself) */
+  int64_t n_parts;                     /* partial slots */
+  int64_t n_splits;
+  const int32_t* splits;               /* [n_splits][4]: head, group, first partial slot, partials */
+  int64_t map_len;
+  const int32_t* item_map;             /* [8][map_len]: item indices per XCD, -1 = none */
+} mmi_work_view;
+
+/* Checks: the items of a row group follow each other in head and group
+ * order and cut its union entries into consecutive ranges that cover it; a
+ * group of one item writes O, a group of several gets consecutive unused
+ * partial slots and exactly one split row naming them; every group with
+ * union entries has items; the item map holds every item exactly once. */
+int mmi_check_work(const mmi_work_view* w);
+
+/* Both checks on a created plan: copies its tables to the host (synchronises
+ * with the plan's stream) and checks every head and the work list. */
+int mmi_plan_check(mmi_plan* plan);
+
 #ifdef __cplusplus
 }
 #endif

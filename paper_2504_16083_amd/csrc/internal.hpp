@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
+
 #include "../../include/mmi.h"
 
 namespace mmi {
@@ -214,5 +216,10 @@ hipError_t launch_sqerr(const void* a, const void* b, int64_t ss, int64_t sh, co
 // k_permute.hip
 hipError_t launch_permute(const void* src, int64_t ss, void* dst, int64_t ds, const int32_t* perm,
                           int64_t n, int64_t row_bytes, int inverse, hipStream_t st);
+
+// ---------------------------------------------------------------- check.hip
+// Host consistency checks of a plan's tables: empty, or the first violation.
+std::string check_index(const mmi_index_view& v);
+std::string check_work(const mmi_work_view& w);
 
 }  // namespace mmi

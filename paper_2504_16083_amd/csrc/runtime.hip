@@ -130,6 +130,7 @@ struct mmi_ctx {
                                    // their head's average union (0: always split to the item target)
   int row_group = 4;               // query blocks per attention work item (1, 2 or 4)
   int live_plans = 0;              // plans created from this context and not destroyed
+  bool debug = false;              // MMI_DEBUG: check every plan's tables, synchronise every execute
   mmi::Allocator alloc;
   int64_t* pinned = nullptr;       // host staging for totals
   size_t pinned_n = 0;
@@ -985,6 +986,83 @@ static void build_item_map(mmi_plan* P, hipStream_t st) {
   P->map_len = len;
 }
 
+// The debug check of a plan: its tables copied to the host, each head's
+// block index and row-group unions, then the work list and item map.
+static void plan_check(mmi_plan* P) {
+  HIPCHK(hipSetDevice(P->ctx->device));
+  HIPCHK(hipStreamSynchronize(P->stream));
+  auto get = [](const int32_t* src, size_t n) {
+    std::vector<int32_t> v(std::max<size_t>(n, 1));
+    if (n) HIPCHK(hipMemcpy(v.data(), src, n * 4, hipMemcpyDeviceToHost));
+    return v;
+  };
+  const int nb_all = (P->S + B - 1) / B;
+  std::vector<int32_t> ngroups(P->Hq);
+  std::vector<std::vector<int32_t>> uptr(P->Hq);
+  for (int h = 0; h < P->Hq; ++h) {
+    const HeadDev& hd = P->heads[h];
+    const HostHead& H = P->hh[h];
+    const std::vector<int32_t> gp = get(hd.gp, 3);
+    const std::vector<int32_t> qp = hd.qperm ? get(hd.qperm, (size_t)hd.nbq * B) : std::vector<int32_t>();
+    const std::vector<int32_t> kp = hd.kperm ? get(hd.kperm, (size_t)hd.nbk * B) : std::vector<int32_t>();
+    const std::vector<int32_t> rp = get(hd.rowptr, hd.nbq + 1), col = get(hd.col, H.nnz);
+    uptr[h] = get(hd.growptr, (size_t)gp[1] + 1);
+    const std::vector<int32_t> ent = get(hd.gcol, H.gnnz);
+    if (rp[hd.nbq] != H.nnz || uptr[h][gp[1]] != H.gnnz)
+      fail(MMI_ERR_INTERNAL, "plan check, head %d: %d / %d entries, the plan sized %lld / %lld", h, rp[hd.nbq],
+           uptr[h][gp[1]], (long long)H.nnz, (long long)H.gnnz);
+    mmi_index_view v{};
+    v.S = P->S;
+    v.n_qblocks = hd.nbq;
+    v.n_kblocks = hd.nbk;
+    v.n_layouts = H.kind == MMI_HEAD_QBOUNDARY && hd.kperm ? hd.nbk / nb_all : 1;
+    v.causal = hd.causal;
+    v.qperm = hd.qperm ? qp.data() : nullptr;
+    v.kperm = hd.kperm ? kp.data() : nullptr;
+    v.row_ptr = rp.data();
+    v.col_idx = col.data();
+    v.group_size = P->R;
+    v.group_stride = gp[0];
+    v.n_groups = gp[1];
+    v.union_ptr = uptr[h].data();
+    v.union_ent = ent.data();
+    const std::string e = check_index(v);
+    if (!e.empty()) fail(MMI_ERR_INTERNAL, "plan check, head %d: %s", h, e.c_str());
+    ngroups[h] = gp[1];
+  }
+  std::vector<WorkItem> items(std::max<int64_t>(P->nitems, 1));
+  std::vector<SplitRow> splits(std::max<int64_t>(P->nsplit, 1));
+  if (P->nitems) HIPCHK(hipMemcpy(items.data(), P->d_items, sizeof(WorkItem) * P->nitems, hipMemcpyDeviceToHost));
+  if (P->nsplit) HIPCHK(hipMemcpy(splits.data(), P->d_splits, sizeof(SplitRow) * P->nsplit, hipMemcpyDeviceToHost));
+  const std::vector<int32_t> map = P->map_len ? get(P->d_item_map, (size_t)8 * P->map_len) : std::vector<int32_t>();
+  std::vector<int32_t> it5((size_t)5 * std::max<int64_t>(P->nitems, 1)), sp4((size_t)4 * std::max<int64_t>(P->nsplit, 1));
+  for (int64_t i = 0; i < P->nitems; ++i) {
+    const WorkItem& w = items[i];
+    const int32_t r[5] = {w.head, w.group, w.e0, w.e1, w.part};
+    std::copy(r, r + 5, it5.begin() + 5 * i);
+  }
+  for (int64_t i = 0; i < P->nsplit; ++i) {
+    const SplitRow& sr = splits[i];
+    const int32_t r[4] = {sr.head, sr.group, sr.part0, sr.nparts};
+    std::copy(r, r + 4, sp4.begin() + 4 * i);
+  }
+  std::vector<const int32_t*> up(P->Hq);
+  for (int h = 0; h < P->Hq; ++h) up[h] = uptr[h].data();
+  mmi_work_view w{};
+  w.n_heads = P->Hq;
+  w.n_groups = ngroups.data();
+  w.union_ptr = up.data();
+  w.n_items = P->nitems;
+  w.items = it5.data();
+  w.n_parts = P->nparts;
+  w.n_splits = P->nsplit;
+  w.splits = sp4.data();
+  w.map_len = P->map_len;
+  w.item_map = map.empty() ? nullptr : map.data();
+  const std::string e = check_work(w);
+  if (!e.empty()) fail(MMI_ERR_INTERNAL, "plan check, work list: %s", e.c_str());
+}
+
 static void plan_execute_impl(mmi_plan* P, const void* q, const void* k, const void* v, void* o, float* lse,
                               hipStream_t st) {
   if (!q || !k || !v || !o) fail(MMI_ERR_INVALID_ARG, "q/k/v/o is NULL");
@@ -1083,6 +1161,7 @@ int mmi_ctx_create(int device, mmi_ctx** out) {
       const int v = atoi(e);
       if (v >= 0) c->split_above_avg = v;
     }
+    if (const char* e = getenv("MMI_DEBUG")) c->debug = e[0] != '\0' && strcmp(e, "0") != 0;
     if (const char* e = getenv("MMI_ROW_GROUP")) {
       const int v = atoi(e);
       if (v == 1 || v == 2 || v == 4) c->row_group = v;
@@ -1114,6 +1193,7 @@ static int create_plan(mmi_ctx* ctx, const mmi_problem* prob, const mmi_head_cfg
     P = new mmi_plan();
     P->scratch = scratch_base;
     plan_create_impl(ctx, prob, cfgs, q, k, (hipStream_t)stream, P);
+    if (ctx->debug) plan_check(P);
   });
   if (rc != MMI_OK) {
     if (P) {
@@ -1142,6 +1222,10 @@ int mmi_plan_execute(mmi_plan* plan, const void* q, const void* k, const void* v
   return guarded([&] {
     if (!plan) fail(MMI_ERR_STATE, "plan is NULL");
     plan_execute_impl(plan, q, k, v, o, lse, (hipStream_t)stream);
+    if (plan->ctx->debug) {   // a failed launch is reported by the call that made it
+      HIPCHK(hipStreamSynchronize((hipStream_t)stream));
+      HIPCHK(hipGetLastError());
+    }
   });
 }
 
@@ -1376,6 +1460,29 @@ int mmi_unpermute_rows(const void* src, int64_t src_stride, void* dst, int64_t d
       fail(MMI_ERR_INVALID_ARG, "rows and strides must be positive multiples of 16 bytes");
     aligned16(src, "src"); aligned16(dst, "dst");
     HIPCHK(launch_permute(src, src_stride, dst, dst_stride, perm, n_src, row_bytes, 1, (hipStream_t)stream));
+  });
+}
+
+int mmi_check_index(const mmi_index_view* v) {
+  return guarded([&] {
+    if (!v) fail(MMI_ERR_INVALID_ARG, "view is NULL");
+    const std::string e = check_index(*v);
+    if (!e.empty()) fail(MMI_ERR_INTERNAL, "%s", e.c_str());
+  });
+}
+
+int mmi_check_work(const mmi_work_view* w) {
+  return guarded([&] {
+    if (!w) fail(MMI_ERR_INVALID_ARG, "view is NULL");
+    const std::string e = check_work(*w);
+    if (!e.empty()) fail(MMI_ERR_INTERNAL, "%s", e.c_str());
+  });
+}
+
+int mmi_plan_check(mmi_plan* plan) {
+  return guarded([&] {
+    if (!plan) fail(MMI_ERR_STATE, "plan is NULL");
+    plan_check(plan);
   });
 }
 

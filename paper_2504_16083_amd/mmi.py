@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(HERE, "libmmi.so")
 
 MAXM = 8
 OK = 0
+ERR_INTERNAL = -7
 EXPORT = dict(qperm=0, kperm=1, row_ptr=2, col_idx=3, v=4, u=5, fold=6, vsel=7, ssel=8, params=9, est_lse=10,
               union_ptr=11, union=12)
 _F32 = {"v", "u", "fold", "est_lse"}
@@ -69,10 +70,27 @@ class mmi_plan_timing(ct.Structure):
                 ("work_items", ct.c_int64), ("loaded_blocks", ct.c_int64), ("device_bytes", ct.c_int64)]
 
 
+I32P = ct.POINTER(ct.c_int32)
+
+
+class mmi_index_view(ct.Structure):
+    _fields_ = [("S", ct.c_int32), ("n_qblocks", ct.c_int32), ("n_kblocks", ct.c_int32),
+                ("n_layouts", ct.c_int32), ("causal", ct.c_int32), ("qperm", I32P), ("kperm", I32P),
+                ("row_ptr", I32P), ("col_idx", I32P), ("group_size", ct.c_int32), ("group_stride", ct.c_int32),
+                ("n_groups", ct.c_int32), ("union_ptr", I32P), ("union_ent", I32P)]
+
+
+class mmi_work_view(ct.Structure):
+    _fields_ = [("n_heads", ct.c_int32), ("n_groups", I32P), ("union_ptr", ct.POINTER(I32P)),
+                ("n_items", ct.c_int64), ("items", I32P), ("n_parts", ct.c_int64), ("n_splits", ct.c_int64),
+                ("splits", I32P), ("map_len", ct.c_int64), ("item_map", I32P)]
+
+
 SYMBOLS = ["mmi_plan_timing_get", "mmi_version", "mmi_status_str", "mmi_last_error", "mmi_ctx_create", "mmi_ctx_destroy",
            "mmi_plan_create", "mmi_plan_execute", "mmi_plan_stats", "mmi_plan_export",
            "mmi_plan_destroy", "mmi_attention", "mmi_dense_attention", "mmi_permute_rows",
-           "mmi_unpermute_rows", "mmi_output_sqerr", "mmi_attention_noalloc"]
+           "mmi_unpermute_rows", "mmi_output_sqerr", "mmi_attention_noalloc", "mmi_check_index",
+           "mmi_check_work", "mmi_plan_check"]
 
 _lib = None
 
@@ -103,6 +121,9 @@ def lib():
             "mmi_permute_rows": ([vp, i64, vp, i64, vp, i64, i64, vp], i32),
             "mmi_unpermute_rows": ([vp, i64, vp, i64, vp, i64, i64, vp], i32),
             "mmi_output_sqerr": ([ct.POINTER(mmi_problem), vp, vp, vp, i32, vp, vp], i32),
+            "mmi_check_index": ([ct.POINTER(mmi_index_view)], i32),
+            "mmi_check_work": ([ct.POINTER(mmi_work_view)], i32),
+            "mmi_plan_check": ([vp], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -269,6 +290,10 @@ class Plan:
                                          ct.byref(need)))
         return out
 
+    def check(self):
+        """Consistency check of the plan's tables on the host (raises MMIError)."""
+        _check(lib().mmi_plan_check(self.h))
+
     def destroy(self):
         if self.h:
             _check(lib().mmi_plan_destroy(self.h))
@@ -343,6 +368,47 @@ def mmi_output_sqerr(prob, a, b, cls, n_class, out, stream=None):
     and b summed over the positions of class c."""
     _check(lib().mmi_output_sqerr(ct.byref(prob.c), _ptr(a), _ptr(b), _ptr(cls), int(n_class), _ptr(out),
                                   _stream(stream)))
+
+
+def _i32(a):
+    """int32 C-contiguous copy (kept alive by the caller) and its pointer, or (None, None)."""
+    if a is None:
+        return None, None
+    arr = np.ascontiguousarray(a, dtype=np.int32)
+    return arr, arr.ctypes.data_as(I32P)
+
+
+def mmi_check_index(S, n_qblocks, n_kblocks, row_ptr, col_idx, qperm=None, kperm=None, n_layouts=1, causal=True,
+                    group_size=0, group_stride=1, union_ptr=None, union_ent=None):
+    """Host consistency check of one head's block index (raises MMIError);
+    union_ptr None skips the row-group checks."""
+    keep = [_i32(x) for x in (qperm, kperm, row_ptr, col_idx, union_ptr, union_ent)]
+    v = mmi_index_view(S=S, n_qblocks=n_qblocks, n_kblocks=n_kblocks, n_layouts=n_layouts, causal=int(causal),
+                       qperm=keep[0][1], kperm=keep[1][1], row_ptr=keep[2][1], col_idx=keep[3][1],
+                       group_size=group_size, group_stride=group_stride,
+                       n_groups=0 if union_ptr is None else len(union_ptr) - 1,
+                       union_ptr=keep[4][1], union_ent=keep[5][1])
+    _check(lib().mmi_check_index(ct.byref(v)))
+
+
+def mmi_check_work(union_ptrs, items, n_parts, splits, item_map):
+    """Host consistency check of a work list: union_ptrs per head, items
+    [n][5] (head, group, e0, e1, partial slot), splits [n][4], item_map [8][len]."""
+    ups = [_i32(u) for u in union_ptrs]
+    ng = np.array([len(u) - 1 for u in union_ptrs], dtype=np.int32)
+    up_arr = (I32P * max(1, len(ups)))(*[p for _, p in ups])
+    it, itp = _i32(np.asarray(items).reshape(-1))
+    sp, spp = _i32(np.asarray(splits).reshape(-1))
+    im = np.asarray(item_map)
+    mp, mpp = _i32(im.reshape(-1))
+    w = mmi_work_view(n_heads=len(ups), n_groups=ng.ctypes.data_as(I32P), union_ptr=up_arr,
+                      n_items=len(it) // 5, items=itp, n_parts=n_parts, n_splits=len(sp) // 4, splits=spp,
+                      map_len=im.shape[1] if im.ndim == 2 else 0, item_map=mpp)
+    _check(lib().mmi_check_work(ct.byref(w)))
+
+
+def mmi_plan_check(plan: Plan):
+    plan.check()
 
 
 @atexit.register

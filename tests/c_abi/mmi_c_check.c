@@ -2,7 +2,8 @@
  *   1. status codes and messages for invalid arguments;
  *   2. a global A-shape head whose window covers every key selects every
  *      causal block, so mmi_attention must equal mmi_dense_attention bitwise;
- *   3. plan statistics of that head (every causal block selected);
+ *   3. plan statistics of that head (every causal block selected) and the
+ *      host consistency checks of its tables;
  *   4. sampled rows of the output against plain causal softmax attention
  *      computed here in double precision (|dO| <= 2e-2, |dLSE| <= 1e-3).
  * Prints "c abi ok" and exits 0 on success. */
@@ -113,6 +114,17 @@ int main(void) {
   CHECK(mmi_plan_create(ctx, &p, cfgs, dq, dk, NULL, &plan));
   mmi_head_stats st;
   CHECK(mmi_plan_stats(plan, 1, &st));
+  CHECK(mmi_plan_check(plan));     /* the plan's tables pass the host consistency checks */
+  {                                /* and a block index with a key block out of range fails them */
+    int32_t rp[2] = {0, 1}, col[1] = {1};
+    mmi_index_view iv;
+    memset(&iv, 0, sizeof iv);
+    iv.S = 64; iv.n_qblocks = 1; iv.n_kblocks = 1; iv.n_layouts = 1; iv.causal = 1;
+    iv.row_ptr = rp; iv.col_idx = col;
+    EXPECT(mmi_check_index(&iv) == MMI_ERR_INTERNAL);
+    col[0] = 0;
+    CHECK(mmi_check_index(&iv));
+  }
   EXPECT(st.kind == MMI_HEAD_GLOBAL && st.nnz_blocks == st.causal_blocks);
   CHECK(mmi_plan_destroy(plan));
 

@@ -21,7 +21,7 @@ def declared():
 
 def test_every_declared_symbol_is_exported():
     names = declared()
-    assert len(names) == 17 and set(names) == set(mmi.SYMBOLS)
+    assert len(names) == 20 and set(names) == set(mmi.SYMBOLS)
     L = mmi.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -35,6 +35,8 @@ def test_struct_sizes_match_header():
     assert ct.sizeof(mmi.mmi_op) == 80
     assert ct.sizeof(mmi.mmi_head_cfg) == 4 + 80 + 8 * 80 + 64 * 80
     assert mmi.mmi_problem.modality.offset == 88 and ct.sizeof(mmi.mmi_problem) == 104
+    assert mmi.mmi_index_view.union_ent.offset == 80 and ct.sizeof(mmi.mmi_index_view) == 88
+    assert mmi.mmi_work_view.item_map.offset == 72 and ct.sizeof(mmi.mmi_work_view) == 80
 
 
 def _create(prob, heads, q=16, k=16):
