@@ -41,7 +41,7 @@ FLOP_PER_BLOCK = 4 * 64 * 64 * 128
 # reported as null.
 TRAFFIC_SOURCES = ("k_attention.hip", "k_blocks.hip", "runtime.hip")
 TRAFFIC = {
-    "0794471d368b0394": {"workload": "cfg4_mm_1m", "fetch_kib": 781994766, "write_kib": 7693171,
+    "db4cb6d645efe5d0": {"workload": "cfg4_mm_1m", "fetch_kib": 777150905, "write_kib": 7480128,
                          "fetch_scale": 1.939, "write_scale": 1.000},
 }
 

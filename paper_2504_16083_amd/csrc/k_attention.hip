@@ -348,8 +348,9 @@ __device__ __forceinline__ void softmax_piece(int pc, f32x16 (&s)[2], float sc, 
 // The three pieces of step t that share no data: QK(t+2) and PV(t) on the
 // matrix cores, softmax(t+1) on the vector ALU. They are written out
 // interleaved (MFMA, then a share of the softmax), because the hardware
-// overlaps vector instructions only with MFMAs of the same wave. MFMA A
-// operands are read from LDS three slots ahead.
+// overlaps vector instructions only with MFMAs of the same wave, and a
+// scheduling barrier after each slot keeps that order. MFMA A operands are
+// read from LDS three slots ahead.
 template <bool QK, bool PV, bool WL>
 __device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, const Stage& vst, f32x16 (&s_qk)[2],
                                            const bf16x8 (&p_cur)[4], f32x16 (&s_sm)[2], bf16x8 (&p_new)[4],
@@ -389,6 +390,9 @@ __device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, cons
     const int pe = (i + 1) * SM_PIECES / (NM > 0 ? NM : 1);
 #pragma unroll
     for (; pc < pe; ++pc) softmax_piece<WL>(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
+    // keep each slot's softmax share next to its MFMA: left to itself the
+    // scheduler bunches the vector work and leaves runs of MFMAs without any
+    __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
   for (; pc < SM_PIECES; ++pc) softmax_piece<WL>(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
