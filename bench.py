@@ -41,7 +41,7 @@ FLOP_PER_BLOCK = 4 * 64 * 64 * 128
 # reported as null.
 TRAFFIC_SOURCES = ("k_attention.hip", "k_blocks.hip", "runtime.hip")
 TRAFFIC = {
-    "db4cb6d645efe5d0": {"workload": "cfg4_mm_1m", "fetch_kib": 777150905, "write_kib": 7480128,
+    "ffa36f506f3b3874": {"workload": "cfg4_mm_1m", "fetch_kib": 531847701, "write_kib": 7697904,
                          "fetch_scale": 1.939, "write_scale": 1.000},
 }
 

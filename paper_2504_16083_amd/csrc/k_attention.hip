@@ -23,7 +23,9 @@
 // softmax), because the vector ALU overlaps only MFMAs of the same wave.
 // Meanwhile block t+3 is written to its stage from registers, the global
 // loads of block t+4 are in flight and the key positions of block t+5 are
-// loading.
+// loading. The two waves of a SIMD stage at opposite ends of the step (one
+// before its products, one after), so that the SIMD's matrix core is fed by
+// one wave while the other waits on its loads.
 // V stays row-major in LDS and is read into the PV operand with the gfx950
 // transpose read (ds_read_b64_tr_b16): in each 16-lane group, output lane i,
 // element e is element i%4 of the 8-byte row addressed by lane 4e + i/4.
@@ -292,6 +294,7 @@ struct WaveState {
   bf16x8 qr[8];
   float m, l, lo;
   int qpos, rb, c, h, vlane;
+  bool late;                  // stages before the products (second wave of a SIMD)
 };
 
 // Mask threshold of a wave's rows: keys above it are masked. A bidirectional
@@ -416,6 +419,14 @@ __device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const KeyS
   const Stage& vst = stg[t & (NSTAGE - 1)];
   const Stage& kst = stg[(t + 2) & (NSTAGE - 1)];
   float alpha = 1.0f;
+  // the second wave of each SIMD stages before its products, the first after
+  // them: the SIMD's MFMAs then overlap one wave's staging
+  auto side = [&]() {
+    if (t + 3 < n) stage_block<R>(stg[(t + 3) & (NSTAGE - 1)], regs, tid);
+    if (t + 4 < n) fetch_block<R>(regs, ks, kpn);
+    if (t + 5 < n) fetch_pos<R, PERM>(kpn, ks, e5 & 0xffff);
+  };
+  if (ws.late) side();
   if (a1) {
     if (needs_mask(e1, ws.rb)) mask_block(stg[(t + 1) & (NSTAGE - 1)], mask_limit(ws, CAUSAL), ws.h, s_sm);
     if (a2 && a0) fused_step<true, true, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
@@ -427,9 +438,7 @@ __device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const KeyS
     if (a0) pv_block(vst, p_cur, ws.vlane, ws.o);
   }
   // stage t+3 (its stage was last read in step t-1), load t+4, positions of t+5
-  if (t + 3 < n) stage_block<R>(stg[(t + 3) & (NSTAGE - 1)], regs, tid);
-  if (t + 4 < n) fetch_block<R>(regs, ks, kpn);
-  if (t + 5 < n) fetch_pos<R, PERM>(kpn, ks, e5 & 0xffff);
+  if (!ws.late) side();
   // O holds P(t)V(t) relative to the old maximum: move it to the new one
   if (a1 && __any(alpha != 1.0f)) {
 #pragma unroll
@@ -505,6 +514,7 @@ __global__ __launch_bounds__(128 * R) __attribute__((amdgpu_waves_per_eu(R == 4 
   const bool upper = wave >= R;
   WaveState ws;
   ws.rb = upper ? (wave - R + R / 2) % R : wave;
+  ws.late = upper;
   const int half = upper ? 1 : 0;
   ws.c = lane & 31;
   ws.h = lane >> 5;
