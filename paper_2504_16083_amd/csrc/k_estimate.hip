@@ -20,10 +20,11 @@
 // registers as the MFMA B operand): each 64-key tile is loaded once by all
 // 512 threads into LDS (the next tile's rows load while the current one is
 // multiplied) and read as the A operand by every set. Pass 2 takes one job
-// per workgroup and reads its K rows straight from HBM into MFMA operands
-// (two tiles of rows in registers: tile t + 2 loads while t and t + 1 are
-// multiplied and reduced); the jobs of a group over one range find it in
-// that XCD's L2.
+// per workgroup and reads its K rows straight from HBM into MFMA operands,
+// each row by one wave (wave w multiplies keys 32 w .. 32 w + 31 of every
+// tile by all 64 rows; two tiles of rows in registers: tile t + 2 loads
+// while t and t + 1 are multiplied and reduced); the jobs of a group over
+// one range find it in that XCD's L2.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -209,7 +210,7 @@ __global__ __launch_bounds__(64) void k_est_merge(const RowSet* sets) {
   rs.lse2[r] = M + fast_log2(L);
 }
 
-constexpr int APITCH = 65;
+constexpr int APITCH = 72;   // floats per key row of A_hat in LDS: conflict-free writes, 16-byte rows
 constexpr int EST_TPW = 8;    // 64-key tiles per workgroup of the score pass
 
 // Each workgroup takes EST_TPW consecutive tiles of one job: the query rows
@@ -220,7 +221,7 @@ constexpr int EST_TPW = 8;    // 64-key tiles per workgroup of the score pass
 // member] is a job index (-1 = none), nrun runs per group.
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void k_est_scores(const EstJob* jobs, const int32_t* order, int ngrp, int nr,
                                                     int nrun, const RowSet* sets, Tensor q, Tensor k) {
-  __shared__ float ahat[B * APITCH];
+  __shared__ __align__(16) float ahat[B * APITCH];
   __shared__ int kposl[B];      // key positions of the current tile, INT_BIG past L_c
   const int64_t lg = run_item(blockIdx.x, nr);
   const int64_t pair = lg / nr;
@@ -233,48 +234,55 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void k
   if (ta >= jb.ntiles) return;
   const int tb = min(ta + EST_TPW, jb.ntiles);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, c = lane & 31, h = lane >> 5;
-  const int r = wave * 32 + c;
-  const int qpos = r < jb.nrows ? jb.row0 + r : -1;
-  const float lse2 = qpos >= 0 ? sets[jb.rowset].lse2[r] : 0.0f;
-  bf16x8 qr[8];
-  load_q_operand(qr, q, jb.head, qpos, h);
+  // wave w multiplies keys 32 w .. 32 w + 31 of each tile by all 64 rows
+  // (each K row is loaded once per workgroup); lane (c, h) holds rows c and
+  // 32 + c as B operands
+  int qpos[2];
+  float lse2[2];
+  bf16x8 qr[2][8];
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf) {
+    const int r = hf * 32 + c;
+    qpos[hf] = r < jb.nrows ? jb.row0 + r : -1;
+    lse2[hf] = qpos[hf] >= 0 ? sets[jb.rowset].lse2[r] : 0.0f;
+    load_q_operand(qr[hf], q, jb.head, qpos[hf], h);
+  }
   auto key_pos = [&](int kap) { return kap < jb.L_c ? (jb.keymap ? jb.keymap[kap] : kap) : -1; };
   // two tiles of K rows in registers: tile t + 2 loads while tiles t and t + 1 are used
-  int kp[2][2];
-  bf16x8 ka[2][2][8];
+  int kp[2];
+  bf16x8 ka[2][8];
   auto fetch = [&](int buf, int t) {
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      kp[buf][kt] = key_pos(t * B + kt * 32 + c);
-      load_key(ka[buf][kt], k, jb.kvh, kp[buf][kt], h);
-    }
+    kp[buf] = key_pos(t * B + wave * 32 + c);
+    load_key(ka[buf], k, jb.kvh, kp[buf], h);
   };
   auto tile = [&](int buf, int t) {
     f32x16 s[2];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) s[kt] = key_product(ka[buf][kt], qr);
-    if (wave == 0 && h == 0) {
-      kposl[c] = kp[buf][0] >= 0 ? kp[buf][0] : INT_BIG;
-      kposl[32 + c] = kp[buf][1] >= 0 ? kp[buf][1] : INT_BIG;
-    }
+    for (int hf = 0; hf < 2; ++hf) s[hf] = key_product(ka[buf], qr[hf]);
+    if (h == 0) kposl[wave * 32 + c] = kp[buf] >= 0 ? kp[buf] : INT_BIG;
     if (t + 2 < tb) fetch(buf, t + 2);
     __syncthreads();
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int kk = kt * 32 + 8 * i + 4 * h + j;   // key index inside the tile
+          const int kk = wave * 32 + 8 * i + 4 * h + j;   // key index inside the tile
           const int kp2 = kposl[kk];
-          const float a = (qpos >= 0 && kp2 <= qpos) ? fast_exp2(s[kt][4 * i + j] * SC - lse2) : 0.0f;
-          ahat[kk * APITCH + r] = a;
+          const float a = (qpos[hf] >= 0 && kp2 <= qpos[hf]) ? fast_exp2(s[hf][4 * i + j] * SC - lse2[hf]) : 0.0f;
+          ahat[kk * APITCH + hf * 32 + c] = a;
         }
     __syncthreads();
     {   // column sums: two threads per key, rows 0-31 and 32-63, then the pair
       const int kk = tid >> 1, half = tid & 1;
+      const float4* src = reinterpret_cast<const float4*>(&ahat[kk * APITCH + 32 * half]);
       float acc = 0.0f;
-      for (int rr = 32 * half; rr < 32 * half + 32; ++rr) acc += ahat[kk * APITCH + rr];
+#pragma unroll
+      for (int x = 0; x < 8; ++x) {
+        const float4 v4 = src[x];
+        acc += v4.x; acc += v4.y; acc += v4.z; acc += v4.w;
+      }
       const float other = __shfl_xor(acc, 1);
       const float tot = half == 0 ? acc + other : other + acc;
       const int kap = t * B + kk;
@@ -284,8 +292,14 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void k
       const int d = tid;
       float acc = 0.0f;
       if (d < 127) {
-        const int rlo = max(0, d - 63), rhi = min(63, d);
-        for (int rr = rlo; rr <= rhi; ++rr) acc += ahat[(rr + 63 - d) * APITCH + rr];
+        // rows rr with key rr + 63 - d inside the tile, ascending; the others add 0
+#pragma unroll 16
+        for (int rr = 0; rr < B; ++rr) {
+          const int kk = rr + 63 - d;
+          const bool in = kk >= 0 && kk < B;
+          const float x = ahat[(in ? kk : 0) * APITCH + rr];
+          acc += in ? x : 0.0f;
+        }
       }
       jb.dpart[(int64_t)t * 128 + d] = acc;
     }
