@@ -535,6 +535,16 @@ def measure(wl, args, ctx, stream, sdpa=False):
             ntiles *= -(-n // x)
         causal_blocks = ntiles * ntiles * wl.Hq
 
+    # causal-useful share of the computed pairs (outside the timed region)
+    plan = mmi.Plan(ctx, prob, wl.heads, q, k, stream)
+    useful = computed_pairs = 0
+    for h in range(wl.Hq):
+        u, c = plan.pair_counts(h)
+        useful += u
+        computed_pairs += c
+    plan.destroy()
+    log(f"pairs: {useful} of {computed_pairs} computed are used")
+
     dense = None
     if not args.no_dense:
         dense_ms = []
@@ -561,7 +571,8 @@ def measure(wl, args, ctx, stream, sdpa=False):
                  stages_ms={k2: avg[k2] for k2 in ("est_ms", "select_ms", "index_ms", "attn_ms", "combine_ms")},
                  blocks={"computed": blocks, "loaded": loaded,
                          ("all_pairs" if natten else "causal"): causal_blocks,
-                         "density": blocks / causal_blocks, "computed_per_load": blocks / max(loaded, 1)}),
+                         "density": blocks / causal_blocks, "computed_per_load": blocks / max(loaded, 1),
+                         "useful_pair_fraction": useful / max(computed_pairs, 1)}),
             q, k, v)
 
 

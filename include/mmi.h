@@ -240,6 +240,14 @@ int mmi_plan_stats(mmi_plan* plan, int head, mmi_head_stats* out);
 int mmi_plan_export(mmi_plan* plan, int head, int what, int slot, void* host_dst,
                     size_t bytes, size_t* needed);
 
+/* Work of one head (Section 4.1 reports attention FLOPs relative to dense):
+ * *computed = query-key pairs in its selected blocks (nnz_blocks x 4096,
+ * every pair of a selected block is computed); *useful = those the output
+ * uses: live (non-padding) query and key rows, k <= q in original positions
+ * (any live pair for a bidirectional head). Synchronises with the plan's
+ * stream; the plan is not changed. */
+int mmi_plan_pair_counts(mmi_plan* plan, int head, int64_t* useful, int64_t* computed);
+
 /* Stage durations (synchronises with the plan's stream). */
 int mmi_plan_timing_get(mmi_plan* plan, mmi_plan_timing* out);
 

@@ -217,6 +217,10 @@ hipError_t launch_sqerr(const void* a, const void* b, int64_t ss, int64_t sh, co
 hipError_t launch_permute(const void* src, int64_t ss, void* dst, int64_t ds, const int32_t* perm,
                           int64_t n, int64_t row_bytes, int inverse, hipStream_t st);
 
+// k_stats.hip: useful query-key pairs of one head's selected blocks, added to *out
+hipError_t launch_pair_count(const HeadDev* heads, int head, int R, int ngroups, unsigned long long* out,
+                             hipStream_t st);
+
 // ---------------------------------------------------------------- check.hip
 // Host consistency checks of a plan's tables: empty, or the first violation.
 std::string check_index(const mmi_index_view& v);

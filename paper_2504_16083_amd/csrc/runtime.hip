@@ -1295,6 +1295,27 @@ int mmi_plan_stats(mmi_plan* P, int head, mmi_head_stats* out) {
   });
 }
 
+int mmi_plan_pair_counts(mmi_plan* P, int head, int64_t* useful, int64_t* computed) {
+  return guarded([&] {
+    if (!P || !useful || !computed) fail(MMI_ERR_INVALID_ARG, "plan/useful/computed is NULL");
+    if (head < 0 || head >= P->Hq) fail(MMI_ERR_INVALID_ARG, "head %d out of range", head);
+    HIPCHK(hipSetDevice(P->ctx->device));
+    HIPCHK(hipStreamSynchronize(P->stream));
+    int32_t gp[2];
+    HIPCHK(hipMemcpy(gp, P->heads[head].gp, sizeof gp, hipMemcpyDeviceToHost));
+    void* d = P->ctx->alloc.get(sizeof(unsigned long long));
+    unsigned long long n = 0;
+    hipError_t e = hipMemcpyAsync(d, &n, sizeof n, hipMemcpyHostToDevice, P->stream);
+    if (e == hipSuccess) e = launch_pair_count(P->d_heads, head, P->R, gp[1], static_cast<unsigned long long*>(d), P->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(&n, d, sizeof n, hipMemcpyDeviceToHost, P->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(P->stream);
+    P->ctx->alloc.put(d, sizeof(unsigned long long));
+    HIPCHK(e);
+    *useful = (int64_t)n;
+    *computed = P->hh[head].nnz * (int64_t)(B * B);
+  });
+}
+
 int mmi_plan_timing_get(mmi_plan* P, mmi_plan_timing* out) {
   return guarded([&] {
     if (!P || !out) fail(MMI_ERR_INVALID_ARG, "plan/out is NULL");

@@ -90,7 +90,7 @@ SYMBOLS = ["mmi_plan_timing_get", "mmi_version", "mmi_status_str", "mmi_last_err
            "mmi_plan_create", "mmi_plan_execute", "mmi_plan_stats", "mmi_plan_export",
            "mmi_plan_destroy", "mmi_attention", "mmi_dense_attention", "mmi_permute_rows",
            "mmi_unpermute_rows", "mmi_output_sqerr", "mmi_attention_noalloc", "mmi_check_index",
-           "mmi_check_work", "mmi_plan_check"]
+           "mmi_check_work", "mmi_plan_check", "mmi_plan_pair_counts"]
 
 _lib = None
 
@@ -124,6 +124,7 @@ def lib():
             "mmi_check_index": ([ct.POINTER(mmi_index_view)], i32),
             "mmi_check_work": ([ct.POINTER(mmi_work_view)], i32),
             "mmi_plan_check": ([vp], i32),
+            "mmi_plan_pair_counts": ([vp, i32, ct.POINTER(ct.c_int64), ct.POINTER(ct.c_int64)], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -290,6 +291,12 @@ class Plan:
                                          ct.byref(need)))
         return out
 
+    def pair_counts(self, head: int):
+        """(useful, computed) query-key pairs of the head's selected blocks."""
+        u, c = ct.c_int64(), ct.c_int64()
+        _check(lib().mmi_plan_pair_counts(self.h, head, ct.byref(u), ct.byref(c)))
+        return u.value, c.value
+
     def check(self):
         """Consistency check of the plan's tables on the host (raises MMIError)."""
         _check(lib().mmi_plan_check(self.h))
@@ -409,6 +416,10 @@ def mmi_check_work(union_ptrs, items, n_parts, splits, item_map):
 
 def mmi_plan_check(plan: Plan):
     plan.check()
+
+
+def mmi_plan_pair_counts(plan: Plan, head: int):
+    return plan.pair_counts(head)
 
 
 @atexit.register

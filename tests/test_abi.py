@@ -21,7 +21,7 @@ def declared():
 
 def test_every_declared_symbol_is_exported():
     names = declared()
-    assert len(names) == 20 and set(names) == set(mmi.SYMBOLS)
+    assert len(names) == 21 and set(names) == set(mmi.SYMBOLS)
     L = mmi.lib()
     for n in names:
         assert hasattr(L, n), n
