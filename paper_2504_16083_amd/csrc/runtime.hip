@@ -1003,6 +1003,9 @@ static void plan_check(mmi_plan* P) {
     const HeadDev& hd = P->heads[h];
     const HostHead& H = P->hh[h];
     const std::vector<int32_t> gp = get(hd.gp, 3);
+    if (gp[0] < 1 || gp[1] < 0 || gp[1] > hd.gcap)
+      fail(MMI_ERR_INTERNAL, "plan check, head %d: row stride %d, %d row groups (capacity %d)", h, gp[0], gp[1],
+           hd.gcap);
     const std::vector<int32_t> qp = hd.qperm ? get(hd.qperm, (size_t)hd.nbq * B) : std::vector<int32_t>();
     const std::vector<int32_t> kp = hd.kperm ? get(hd.kperm, (size_t)hd.nbk * B) : std::vector<int32_t>();
     const std::vector<int32_t> rp = get(hd.rowptr, hd.nbq + 1), col = get(hd.col, H.nnz);
