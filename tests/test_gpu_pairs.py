@@ -90,3 +90,18 @@ def test_pair_counts_natten(ctx):
              C.global_head(C.natten((3, 30, 32), (1, 1, 1), (1, 4, 16)))]
     say("[gpu] pair counts NATTEN")
     _check(ctx, S, 2, 1, None, heads, q, k)
+
+
+@pytest.mark.parametrize("S", [1, 63, 65])
+def test_pair_counts_tiny(ctx, S):
+    """One token to just over one block, every global op kind (padding rows
+    and keys in the last block)."""
+    g = torch.Generator().manual_seed(S)
+    q = torch.randn(S, 8, 128, generator=g).to(torch.bfloat16).cuda()
+    k = torch.randn(S, 2, 128, generator=g).to(torch.bfloat16).cuda()
+    heads = [C.global_head(C.dense()), C.global_head(C.ashape(1, 4)), C.global_head(C.vslash(3, 2)),
+             C.global_head(C.grid(1, 8)), C.global_head(C.trishape(1, 3, 2)), C.global_head(C.sf_fixed(5, 3)),
+             C.global_head(C.sf_strided(2, 7)),
+             C.global_head(C.natten((1, 1, S), (1, 1, 1 if S < 3 else 3), (1, 1, 64)))]
+    say(f"[gpu] pair counts S={S}")
+    _check(ctx, S, 8, 2, None, heads, q, k)
