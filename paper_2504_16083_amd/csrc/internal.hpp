@@ -164,7 +164,9 @@ hipError_t launch_est_scores(const EstJob* jobs, int njobs, const int32_t* order
 hipError_t launch_est_udiag(const EstJob* jobs, int njobs, int max_L, hipStream_t st);
 // k_select.hip
 hipError_t launch_grid_search(const GridJob* jobs, int njobs, int max_cands, hipStream_t st);
-hipError_t launch_topk(const TopkJob* jobs, int njobs, hipStream_t st);
+// scr: int32 scratch of topk_scratch_ints(njobs) entries (initialised by the launch)
+size_t topk_scratch_ints(int njobs);
+hipError_t launch_topk(const TopkJob* jobs, int njobs, int32_t* scr, hipStream_t st);
 // k_blocks.hip
 hipError_t launch_key_summaries(const HeadDev* heads, int nheads, OpDev* ops, int nops,
                                 Groups g, int max_nbk, int max_sel, hipStream_t st);

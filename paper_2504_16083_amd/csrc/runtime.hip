@@ -841,7 +841,8 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   HIPCHK(launch_est_udiag(d_jobs, (int)bd.jobs.size(), bd.max_L, st));
   mark(P, 1, st);
   HIPCHK(launch_grid_search(d_g, (int)bd.gjobs.size(), bd.max_cands, st));
-  HIPCHK(launch_topk(d_t, (int)bd.tjobs.size(), st));
+  int32_t* d_tscr = dalloc<int32_t>(P, topk_scratch_ints((int)bd.tjobs.size()));
+  HIPCHK(launch_topk(d_t, (int)bd.tjobs.size(), d_tscr, st));
   mark(P, 2, st);
 
   // permutations, key summaries, block counts
