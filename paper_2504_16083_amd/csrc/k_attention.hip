@@ -272,22 +272,6 @@ __device__ __forceinline__ void softmax_block(f32x16 (&s)[2], float sc, float& m
   lo = lo * alpha + xhalf_sum(ro);
 }
 
-// O^T += V^T P^T; the V^T operand comes from row-major V by transpose reads.
-__device__ __forceinline__ void pv_block(const Stage& st, const bf16x8 (&pb)[4], int vlane, f32x16 (&o)[4]) {
-#pragma unroll
-  for (int stp = 0; stp < 4; ++stp) {
-    const int kt = stp >> 1, half = stp & 1;
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
-      const uint16_t* p0 = &st.v[vlane + (32 * kt + 16 * half) * VPITCH + 32 * dt];
-      const bf16x4 lo = tr_read(p0);
-      const bf16x4 hi = tr_read(p0 + 8 * VPITCH);
-      const bf16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      o[dt] = mfma32(va, pb[stp], o[dt]);
-    }
-  }
-}
-
 // Per-wave state of the block loop.
 struct WaveState {
   f32x16 o[4];
@@ -349,12 +333,15 @@ __device__ __forceinline__ void softmax_piece(int pc, f32x16 (&s)[2], float sc, 
 }
 
 // The three pieces of step t that share no data: QK(t+2) and PV(t) on the
-// matrix cores, softmax(t+1) on the vector ALU. They are written out
+// matrix cores, softmax(t+1) on the vector ALU (SM). They are written out
 // interleaved (MFMA, then a share of the softmax), because the hardware
 // overlaps vector instructions only with MFMAs of the same wave, and a
 // scheduling barrier after each slot keeps that order. MFMA A operands are
-// read from LDS three slots ahead.
-template <bool QK, bool PV, bool WL>
+// read from LDS three slots ahead, also in steps without a softmax (a wave
+// whose member skips block t+1), where an operand read right before each
+// MFMA would leave every MFMA waiting for LDS; those steps keep the operands
+// in the P buffer of block t+1, which the member does not use.
+template <bool QK, bool PV, bool SM, bool WL>
 __device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, const Stage& vst, f32x16 (&s_qk)[2],
                                            const bf16x8 (&p_cur)[4], f32x16 (&s_sm)[2], bf16x8 (&p_new)[4],
                                            float sc, float& alpha) {
@@ -375,7 +362,10 @@ __device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, cons
     const bf16x4 hi = tr_read(p0 + 8 * VPITCH);
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   };
-  bf16x8 opa[AHEAD + 1];
+  // without a softmax the P buffer of block t+1 is free (the member skips
+  // that block) and holds the operands in flight
+  bf16x8 opa_own[AHEAD + 1];
+  bf16x8* opa = SM ? opa_own : p_new;
 #pragma unroll
   for (int i = 0; i < AHEAD && i < NM; ++i) opa[i] = operand(i);
   int pc = 0;
@@ -390,15 +380,19 @@ __device__ __forceinline__ void fused_step(WaveState& ws, const Stage& kst, cons
       const int j = i - NQ, stp = j >> 2, dt = j & 3;
       ws.o[dt] = mfma32(av, p_cur[stp], ws.o[dt]);
     }
-    const int pe = (i + 1) * SM_PIECES / (NM > 0 ? NM : 1);
+    if constexpr (SM) {
+      const int pe = (i + 1) * SM_PIECES / (NM > 0 ? NM : 1);
 #pragma unroll
-    for (; pc < pe; ++pc) softmax_piece<WL>(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
+      for (; pc < pe; ++pc) softmax_piece<WL>(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
+    }
     // keep each slot's softmax share next to its MFMA: left to itself the
     // scheduler bunches the vector work and leaves runs of MFMAs without any
     __builtin_amdgcn_sched_barrier(0);
   }
+  if constexpr (SM) {
 #pragma unroll
-  for (; pc < SM_PIECES; ++pc) softmax_piece<WL>(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
+    for (; pc < SM_PIECES; ++pc) softmax_piece<WL>(pc, s_sm, sc, ws.m, ws.l, ws.lo, p_new, alpha, st);
+  }
 }
 
 // Step t. Entries e0..e2 are the union entries t..t+2 (0 past the end): key
@@ -429,13 +423,14 @@ __device__ __forceinline__ void block_step(WaveState& ws, Stage* stg, const KeyS
   if (ws.late) side();
   if (a1) {
     if (needs_mask(e1, ws.rb)) mask_block(stg[(t + 1) & (NSTAGE - 1)], mask_limit(ws, CAUSAL), ws.h, s_sm);
-    if (a2 && a0) fused_step<true, true, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
-    else if (a2) fused_step<true, false, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
-    else if (a0) fused_step<false, true, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
-    else fused_step<false, false, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    if (a2 && a0) fused_step<true, true, true, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    else if (a2) fused_step<true, false, true, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    else if (a0) fused_step<false, true, true, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    else fused_step<false, false, true, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
   } else {
-    if (a2) qk_block(kst, ws.qr, ws.c, ws.h, s_qk);
-    if (a0) pv_block(vst, p_cur, ws.vlane, ws.o);
+    if (a2 && a0) fused_step<true, true, false, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    else if (a2) fused_step<true, false, false, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
+    else if (a0) fused_step<false, true, false, WL>(ws, kst, vst, s_qk, p_cur, s_sm, p_new, sc, alpha);
   }
   // stage t+3 (its stage was last read in step t-1), load t+4, positions of t+5
   if (!ws.late) side();
