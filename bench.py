@@ -41,7 +41,7 @@ FLOP_PER_BLOCK = 4 * 64 * 64 * 128
 # reported as null.
 TRAFFIC_SOURCES = ("k_attention.hip", "k_blocks.hip", "runtime.hip")
 TRAFFIC = {
-    "1d1f8849b9611c2b": {"workload": "cfg4_mm_1m", "fetch_kib": 544213357, "write_kib": 7697809,
+    "7ffd9d195603e983": {"workload": "cfg4_mm_1m", "fetch_kib": 535559839, "write_kib": 7699623,
                          "fetch_scale": 1.939, "write_scale": 1.000},
 }
 
