@@ -398,8 +398,8 @@ def permute_main(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU; multi-GPU sharding is a design "
-                                   "note only (heads shard with no exchange)", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "this library and benchmark run on exactly one GPU; multi-GPU sharding "
+                                   "is a design note only (heads shard with no exchange)", "n_gpus": args.gpus}))
         sys.exit(2)
     if args.workload == "search":
         search_main(args)

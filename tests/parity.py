@@ -109,8 +109,8 @@ def full_check(ctx, S, Hq, Hkv, modality, heads, q, k, v, rows=None, heads_to_ch
 
 
 def _workers():
-    """Oracle worker processes: the host's cores, at most 12 (the GPU machine
-    grants one GPU's share of its CPUs; this process keeps the GPU)."""
+    """Oracle worker processes: the host's cores, at most 12 (a one-GPU host
+    share holds about 16 cores; this process keeps the GPU)."""
     n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
     return max(1, min(12, n))
 
