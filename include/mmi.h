@@ -301,6 +301,64 @@ int mmi_unpermute_rows(const void* src, int64_t src_stride, void* dst, int64_t d
 int mmi_output_sqerr(const mmi_problem* prob, const void* a, const void* b, const uint8_t* cls,
                      int32_t n_class, double* out, void* stream);
 
+/* ------------------------------------------------------------ pattern search
+ * Modality-aware offline pattern search (Appendix A, Algorithm 4; the search
+ * space of Appendix C.5) for every head of one layer on a calibration sample
+ * (q, k, v device bf16 laid out as in `prob`; prob->modality on the host).
+ * Every candidate configuration is one plan of this library for all heads,
+ * executed on the sample: its cost over a set of query rows is the blocks
+ * its plan selects there (mmi_head_stats.blocks_by_modality: the work the
+ * attention kernel runs), its error the squared difference of its output
+ * from a reference output over those rows (mmi_output_sqerr). A candidate is
+ * admissible iff its cost does not exceed the cost of `target` (the FLOPs
+ * target pattern, e.g. A-shape with 1k sink and 4k local tokens) over the
+ * same rows in the same coordinates; the choice is the admissible candidate
+ * of smallest error (the earlier one on equal errors), else the target.
+ * With the n modalities present in the sample, in ascending id:
+ *   1. intra, per modality m: 2D-Boundary heads whose cross pairs select
+ *      nothing, candidate c on every modality; reference: dense intra ops;
+ *      rows: modality m.
+ *   2. cross, in rounds r = 1 .. n-1: 2D-Boundary heads with the chosen
+ *      intra ops, cross candidate x on the pairs (mods[i], mods[(i+r) % n]),
+ *      the other pairs DENSE; reference: dense causal attention; cost: the
+ *      pair's blocks; budget: mods[i]'s step-1 budget minus the cost of its
+ *      chosen intra op; none admissible -> NONE on that pair.
+ *   3. inter: the best global op (chosen as in step 1 over all rows, budget
+ *      = the global target head's cost), the Q-Boundary head with the chosen
+ *      intra ops, the 2D-Boundary head with the chosen intra and cross ops;
+ *      the smallest error among those within that budget (in that order on
+ *      ties), else the cheapest.
+ * cands[n_cands]: intra candidates in table order (n_cands >= 0); xc[n_xc]:
+ * cross candidates (NONE, VERT, DENSE); out: host [Hq], the chosen
+ * configuration of every head. Builds 8 + 2 n_cands + (n - 1) n_xc plans on
+ * `stream` and synchronises with it; allocates device buffers for two
+ * outputs (2 S Hq 128 bytes each) for the duration of the call. `report`
+ * (or NULL) receives the search's steps: each array may be NULL; the index
+ * i is the position of a modality in report->mods. */
+typedef struct mmi_search_report {
+  int32_t n_mod;                        /* out: modalities present */
+  int32_t mods[MMI_MAX_MODALITIES];     /* out: their ids ascending, -1 after n_mod */
+  int64_t plans;                        /* out: plans built */
+  int64_t* budget1;     /* [Hq][8]: target cost of modality i's rows (step 1) */
+  int64_t* step1_cost;  /* [Hq][n_cands][8] */
+  double* step1_err;    /* [Hq][n_cands][8] */
+  int32_t* intra;       /* [Hq][8]: chosen intra candidate of modality i, -1 = target */
+  int64_t* step2_cost;  /* [Hq][7][n_xc][8]: round r-1, candidate x, rows of modality i */
+  double* step2_err;    /* [Hq][7][n_xc][8] */
+  int32_t* cross;       /* [Hq][8][8]: chosen cross candidate of pair (i, j), -1 = NONE */
+  int64_t* budget3;     /* [Hq]: cost of the global target head */
+  int64_t* step3g_cost; /* [Hq][n_cands]: global heads, all rows */
+  double* step3g_err;   /* [Hq][n_cands] */
+  int32_t* global;      /* [Hq]: chosen global candidate, -1 = target */
+  int64_t* step3_cost;  /* [Hq][3]: global, Q-Boundary, 2D-Boundary */
+  double* step3_err;    /* [Hq][3] */
+  int32_t* kind;        /* [Hq]: chosen kind, 0 global, 1 Q-Boundary, 2 2D-Boundary */
+} mmi_search_report;
+
+int mmi_search(mmi_ctx* ctx, const mmi_problem* prob, const void* q, const void* k, const void* v,
+               const mmi_op* cands, int32_t n_cands, const mmi_op* xc, int32_t n_xc, const mmi_op* target,
+               void* stream, mmi_head_cfg* out, mmi_search_report* report);
+
 /* ------------------------------------------------------------ debug checks
  * Host-side consistency checks of a plan's tables: when they pass, every
  * index the attention kernel derives from the tables (permutation slots,

@@ -6,11 +6,19 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <stdexcept>
 #include <string>
 
 #include "../../include/mmi.h"
 
 namespace mmi {
+
+// Error of a host call: the C entry points turn it into their status code
+// and the thread's last-error text.
+struct Error : std::runtime_error {
+  int code;
+  Error(int c, const std::string& m) : std::runtime_error(m), code(c) {}
+};
 
 constexpr int B = 64;            // block size (rows and keys)
 constexpr int D = 128;           // head dim
@@ -227,5 +235,11 @@ hipError_t launch_pair_count(const HeadDev* heads, int head, int R, int ngroups,
 // Host consistency checks of a plan's tables: empty, or the first violation.
 std::string check_index(const mmi_index_view& v);
 std::string check_work(const mmi_work_view& w);
+
+// The pattern search of Algorithm 4 (search.hip) over plans of this library;
+// the problem is already validated, out has prob.Hq entries.
+void search_layer(mmi_ctx* ctx, const mmi_problem& prob, const void* q, const void* k, const void* v,
+                  const mmi_op* cands, int nc, const mmi_op* xc, int nx, const mmi_op& target, hipStream_t st,
+                  mmi_head_cfg* out, mmi_search_report* rep);
 
 }  // namespace mmi

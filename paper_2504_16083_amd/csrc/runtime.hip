@@ -22,11 +22,6 @@
 namespace mmi {
 
 // ------------------------------------------------------------------ errors
-struct Error : std::runtime_error {
-  int code;
-  Error(int c, const std::string& m) : std::runtime_error(m), code(c) {}
-};
-
 static thread_local std::string g_last_error;
 
 [[noreturn]] static void fail(int code, const char* fmt, ...) {
@@ -1523,6 +1518,19 @@ int mmi_output_sqerr(const mmi_problem* prob, const void* a, const void* b, cons
       fail(MMI_ERR_INVALID_ARG, "n_class must be in [1, %d]", MMI_MAX_MODALITIES);
     aligned16(a, "a"); aligned16(b, "b");
     HIPCHK(launch_sqerr(a, b, p.o_stride_s, p.o_stride_h, cls, n_class, (int)p.S, p.Hq, out, (hipStream_t)stream));
+  });
+}
+
+int mmi_search(mmi_ctx* ctx, const mmi_problem* prob, const void* q, const void* k, const void* v,
+               const mmi_op* cands, int32_t n_cands, const mmi_op* xc, int32_t n_xc, const mmi_op* target,
+               void* stream, mmi_head_cfg* out, mmi_search_report* report) {
+  return guarded([&] {
+    if (!ctx || !q || !k || !v || !target || !out) fail(MMI_ERR_INVALID_ARG, "NULL pointer");
+    if (n_cands < 0 || n_xc < 0 || (n_cands > 0 && !cands) || (n_xc > 0 && !xc))
+      fail(MMI_ERR_INVALID_ARG, "candidate lists: negative count or NULL array");
+    const mmi_problem p = normalise(prob);
+    HIPCHK(hipSetDevice(ctx->device));
+    search_layer(ctx, p, q, k, v, cands, n_cands, xc, n_xc, *target, (hipStream_t)stream, out, report);
   });
 }
 

@@ -86,7 +86,18 @@ class mmi_work_view(ct.Structure):
                 ("splits", I32P), ("map_len", ct.c_int64), ("item_map", I32P)]
 
 
-SYMBOLS = ["mmi_plan_timing_get", "mmi_version", "mmi_status_str", "mmi_last_error", "mmi_ctx_create", "mmi_ctx_destroy",
+I64P, F64P = ct.POINTER(ct.c_int64), ct.POINTER(ct.c_double)
+
+
+class mmi_search_report(ct.Structure):
+    _fields_ = [("n_mod", ct.c_int32), ("mods", ct.c_int32 * MAXM), ("plans", ct.c_int64),
+                ("budget1", I64P), ("step1_cost", I64P), ("step1_err", F64P), ("intra", I32P),
+                ("step2_cost", I64P), ("step2_err", F64P), ("cross", I32P), ("budget3", I64P),
+                ("step3g_cost", I64P), ("step3g_err", F64P), ("global_", I32P), ("step3_cost", I64P),
+                ("step3_err", F64P), ("kind", I32P)]
+
+
+SYMBOLS = ["mmi_search", "mmi_plan_timing_get", "mmi_version", "mmi_status_str", "mmi_last_error", "mmi_ctx_create", "mmi_ctx_destroy",
            "mmi_plan_create", "mmi_plan_execute", "mmi_plan_stats", "mmi_plan_export",
            "mmi_plan_destroy", "mmi_attention", "mmi_dense_attention", "mmi_permute_rows",
            "mmi_unpermute_rows", "mmi_output_sqerr", "mmi_attention_noalloc", "mmi_check_index",
@@ -125,6 +136,9 @@ def lib():
             "mmi_check_work": ([ct.POINTER(mmi_work_view)], i32),
             "mmi_plan_check": ([vp], i32),
             "mmi_plan_pair_counts": ([vp, i32, ct.POINTER(ct.c_int64), ct.POINTER(ct.c_int64)], i32),
+            "mmi_search": ([vp, ct.POINTER(mmi_problem), vp, vp, vp, ct.POINTER(mmi_op), i32, ct.POINTER(mmi_op),
+                            i32, ct.POINTER(mmi_op), vp, ct.POINTER(mmi_head_cfg),
+                            ct.POINTER(mmi_search_report)], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -375,6 +389,35 @@ def mmi_output_sqerr(prob, a, b, cls, n_class, out, stream=None):
     and b summed over the positions of class c."""
     _check(lib().mmi_output_sqerr(ct.byref(prob.c), _ptr(a), _ptr(b), _ptr(cls), int(n_class), _ptr(out),
                                   _stream(stream)))
+
+
+def mmi_search(ctx, prob, q, k, v, cands, xc, target, stream=None):
+    """Algorithm 4 for every head (the C call mmi_search). cands / xc: ops in
+    table order; target: the FLOPs target op. Returns (the chosen
+    mmi_head_cfg per head, the report's arrays as numpy arrays)."""
+    Hq = prob.c.Hq
+    nc, nx = len(cands), len(xc)
+    ca = (mmi_op * max(nc, 1))(*[op_struct(o) for o in cands])
+    xa = (mmi_op * max(nx, 1))(*[op_struct(o) for o in xc])
+    tgt = op_struct(target)
+    out = (mmi_head_cfg * Hq)()
+    arrays = {"budget1": (np.int64, (Hq, MAXM)), "step1_cost": (np.int64, (Hq, nc, MAXM)),
+              "step1_err": (np.float64, (Hq, nc, MAXM)), "intra": (np.int32, (Hq, MAXM)),
+              "step2_cost": (np.int64, (Hq, MAXM - 1, nx, MAXM)), "step2_err": (np.float64, (Hq, MAXM - 1, nx, MAXM)),
+              "cross": (np.int32, (Hq, MAXM, MAXM)), "budget3": (np.int64, (Hq,)),
+              "step3g_cost": (np.int64, (Hq, nc)), "step3g_err": (np.float64, (Hq, nc)),
+              "global_": (np.int32, (Hq,)), "step3_cost": (np.int64, (Hq, 3)), "step3_err": (np.float64, (Hq, 3)),
+              "kind": (np.int32, (Hq,))}
+    rep = mmi_search_report()
+    got = {}
+    for name, (dt, shape) in arrays.items():
+        a = got[name] = np.zeros(shape, dt)
+        ptype = {np.int64: I64P, np.int32: I32P, np.float64: F64P}[dt]
+        setattr(rep, name, a.ctypes.data_as(ptype))
+    _check(lib().mmi_search(ctx.h, ct.byref(prob.c), _ptr(q), _ptr(k), _ptr(v), ca, nc, xa, nx, ct.byref(tgt),
+                            _stream(stream), out, ct.byref(rep)))
+    got["n_mod"], got["mods"], got["plans"] = rep.n_mod, list(rep.mods)[:rep.n_mod], rep.plans
+    return list(out), got
 
 
 def _i32(a):

@@ -5,7 +5,10 @@
  *   3. plan statistics of that head (every causal block selected) and the
  *      host consistency checks of its tables;
  *   4. sampled rows of the output against plain causal softmax attention
- *      computed here in double precision (|dO| <= 2e-2, |dLSE| <= 1e-3).
+ *      computed here in double precision (|dO| <= 2e-2, |dLSE| <= 1e-3);
+ *   5. the pattern search (Algorithm 4) over two intra candidates: the
+ *      number of plans it builds, and a chosen configuration that is the
+ *      one its report names.
  * Prints "c abi ok" and exits 0 on success. */
 #include <hip/hip_runtime_api.h>
 #include <math.h>
@@ -98,6 +101,7 @@ int main(void) {
   cfgs[0].global.kind = 99;
   EXPECT(mmi_plan_create(ctx, &p, cfgs, dq, dk, NULL, &plan) == MMI_ERR_BAD_CONFIG);
   cfgs[0].global.kind = MMI_OP_ASHAPE;
+  EXPECT(mmi_search(ctx, &p, dq, dk, dv, NULL, 0, NULL, 0, NULL, NULL, cfgs, NULL) == MMI_ERR_INVALID_ARG);
 
   /* 2. full-window A-shape == dense, bitwise */
   CHECK(mmi_attention(ctx, &p, cfgs, dq, dk, dv, do1, dl1, NULL));
@@ -158,6 +162,34 @@ int main(void) {
   }
   printf("max |dO| %.3g, max rel |dLSE| %.3g\n", max_do, max_dl);
   EXPECT(max_do <= 2e-2 && max_dl <= 1e-3);
+
+  /* 5. search: one modality, intra candidates {dense, A-shape(64, 128)},
+   * no cross candidates, target A-shape(64, 256): 8 + 2*2 + 0 plans */
+  {
+    mmi_op cand[2], target;
+    memset(cand, 0, sizeof cand);
+    memset(&target, 0, sizeof target);
+    cand[0].kind = MMI_OP_DENSE;
+    cand[1].kind = MMI_OP_ASHAPE; cand[1].sink = 64; cand[1].local = 128;
+    target.kind = MMI_OP_ASHAPE; target.sink = 64; target.local = 256;
+    mmi_head_cfg* chosen = calloc(Hq, sizeof(mmi_head_cfg));
+    int32_t kind[8], glob[8], intra[8 * MMI_MAX_MODALITIES];
+    int64_t budget3[8], cost3[8 * 3];
+    mmi_search_report rep;
+    memset(&rep, 0, sizeof rep);
+    rep.kind = kind; rep.global = glob; rep.intra = intra; rep.budget3 = budget3; rep.step3_cost = cost3;
+    EXPECT(Hq <= 8);
+    CHECK(mmi_search(ctx, &p, dq, dk, dv, cand, 2, NULL, 0, &target, NULL, chosen, &rep));
+    EXPECT(rep.plans == 8 + 2 * 2 && rep.n_mod == 1 && rep.mods[0] == 0 && rep.mods[1] == -1);
+    for (int h = 0; h < Hq; ++h) {
+      EXPECT(kind[h] >= 0 && kind[h] <= 2 && chosen[h].kind == kind[h]);
+      /* dense exceeds the target's cost over all rows, so a chosen global op is the A-shape */
+      EXPECT(glob[h] == 1 && intra[h * MMI_MAX_MODALITIES] == 1);
+      if (kind[h] == MMI_HEAD_GLOBAL) EXPECT(chosen[h].global.kind == MMI_OP_ASHAPE && chosen[h].global.local == 128);
+      EXPECT(cost3[h * 3 + kind[h]] <= budget3[h]);
+    }
+    free(chosen);
+  }
 
   CHECK(mmi_ctx_destroy(ctx));
   HCHECK(hipFree(dq)); HCHECK(hipFree(dk)); HCHECK(hipFree(dv)); HCHECK(hipFree(do1)); HCHECK(hipFree(do2));

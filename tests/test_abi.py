@@ -21,7 +21,7 @@ def declared():
 
 def test_every_declared_symbol_is_exported():
     names = declared()
-    assert len(names) == 21 and set(names) == set(mmi.SYMBOLS)
+    assert len(names) == 22 and set(names) == set(mmi.SYMBOLS)
     L = mmi.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -37,6 +37,7 @@ def test_struct_sizes_match_header():
     assert mmi.mmi_problem.modality.offset == 88 and ct.sizeof(mmi.mmi_problem) == 104
     assert mmi.mmi_index_view.union_ent.offset == 80 and ct.sizeof(mmi.mmi_index_view) == 88
     assert mmi.mmi_work_view.item_map.offset == 72 and ct.sizeof(mmi.mmi_work_view) == 80
+    assert mmi.mmi_search_report.kind.offset == 152 and ct.sizeof(mmi.mmi_search_report) == 160
 
 
 def _create(prob, heads, q=16, k=16):
@@ -44,6 +45,22 @@ def _create(prob, heads, q=16, k=16):
     h = ct.c_void_p()
     return mmi.lib().mmi_plan_create(None, ct.byref(prob.c), cfgs, ct.c_void_p(q), ct.c_void_p(k), None,
                                      ct.byref(h))
+
+
+def test_search_arguments_without_device():
+    """mmi_search refuses NULL pointers and bad candidate lists before it
+    touches the context or the device."""
+    L = mmi.lib()
+    prob = mmi.Problem(100, 2, 1)
+    tgt = mmi.op_struct(C.ashape(64, 256))
+    cands = (mmi.mmi_op * 1)(mmi.op_struct(C.dense()))
+    out = (mmi.mmi_head_cfg * 2)()
+    dev = ct.c_void_p(1 << 20)                  # never dereferenced: the call fails first
+    assert L.mmi_search(None, ct.byref(prob.c), dev, dev, dev, cands, 1, None, 0, ct.byref(tgt), None, out,
+                        None) == -1
+    assert "NULL" in mmi.mmi_last_error()
+    assert L.mmi_search(None, ct.byref(prob.c), dev, dev, dev, cands, 1, None, 0, None, None, out,
+                        None) == -1
 
 
 def test_validation_codes_without_device():

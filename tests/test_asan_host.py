@@ -42,5 +42,6 @@ def test_validation_under_asan():
     _run("import test_abi\n"
          "test_abi.test_every_declared_symbol_is_exported()\n"
          "test_abi.test_struct_sizes_match_header()\n"
-         "test_abi.test_validation_codes_without_device()\n", timeout=300)
+         "test_abi.test_validation_codes_without_device()\n"
+         "test_abi.test_search_arguments_without_device()\n", timeout=300)
 

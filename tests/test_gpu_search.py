@@ -53,6 +53,9 @@ def test_search_matches_oracle():
     finally:
         ctx.close()
     say(f"[gpu] search: {nplans} plans; kinds {[r.kind for r in reps]}")
+    assert nplans == 8 + 2 * len(cands) + len(xc)
+    for h in range(2):    # the configuration the C call chose is the one the records name
+        assert bytes(mmi._head_cfg(heads[h])) == bytes(reps[h].abi_cfg), h
     rows = {m: int((mod == m).sum()) for m in (0, 1)}
     ties = 0
     for h in range(2):
