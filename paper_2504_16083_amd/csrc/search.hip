@@ -50,7 +50,11 @@ void hipcall(hipError_t e, const char* what) {
 
 struct DevBuf {
   void* p = nullptr;
-  explicit DevBuf(size_t bytes) { hipcall(hipMalloc(&p, std::max<size_t>(bytes, 1)), "hipMalloc"); }
+  explicit DevBuf(size_t bytes) {
+    const hipError_t e = hipMalloc(&p, std::max<size_t>(bytes, 1));
+    if (e == hipErrorOutOfMemory) throw Error(MMI_ERR_OOM, "device allocation of the search's buffers failed");
+    hipcall(e, "hipMalloc");
+  }
   ~DevBuf() {
     if (p) (void)hipFree(p);
   }
