@@ -210,7 +210,8 @@ __global__ __launch_bounds__(64) void k_est_merge(const RowSet* sets) {
   rs.lse2[r] = M + fast_log2(L);
 }
 
-constexpr int APITCH = 72;   // floats per key row of A_hat in LDS: conflict-free writes, 16-byte rows
+constexpr int APITCH = 65;   // floats per key row of A_hat in LDS: odd, so that the lanes of the
+                             // diagonal sums (one diagonal each) read distinct banks
 constexpr int EST_TPW = 8;    // 64-key tiles per workgroup of the score pass
 
 // Each workgroup takes EST_TPW consecutive tiles of one job: the query rows
@@ -276,13 +277,10 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void k
     __syncthreads();
     {   // column sums: two threads per key, rows 0-31 and 32-63, then the pair
       const int kk = tid >> 1, half = tid & 1;
-      const float4* src = reinterpret_cast<const float4*>(&ahat[kk * APITCH + 32 * half]);
+      const float* src = &ahat[kk * APITCH + 32 * half];
       float acc = 0.0f;
 #pragma unroll
-      for (int x = 0; x < 8; ++x) {
-        const float4 v4 = src[x];
-        acc += v4.x; acc += v4.y; acc += v4.z; acc += v4.w;
-      }
+      for (int x = 0; x < 32; ++x) acc += src[x];
       const float other = __shfl_xor(acc, 1);
       const float tot = half == 0 ? acc + other : other + acc;
       const int kap = t * B + kk;
