@@ -156,3 +156,25 @@ def test_search_calibration_costs():
         say(f"  {name}: " + rep.line())
         assert rep.ties, (name, got, want)
         assert sum(rep.nnz.values()) == sum(got.values())
+
+
+def test_search_reports_a_bad_candidate():
+    """A candidate the library rejects stops the search with the plan's own
+    status and message (here an op kind out of range), and the context stays
+    usable: the same search with valid candidates runs after it."""
+    from paper_2504_16083_amd import mmi
+    from paper_2504_16083_amd import search as GS
+    mod, (Q, K, V) = sample()
+    cands, xc, target = small_space()
+    q, k, v = (torch.from_numpy(x).to(torch.bfloat16).cuda() for x in (Q, K, V))
+    bad = C.Op(kind=99)
+    ctx = mmi.Ctx(0)
+    try:
+        with pytest.raises(mmi.MMIError) as e:
+            GS.search(ctx, S, 2, 1, mod, q, k, v, [("bad", bad)] + list(cands), xc, target)
+        assert e.value.status == -3 and len(str(e.value)) > 0, str(e.value)
+        heads, reps, nplans = GS.search(ctx, S, 2, 1, mod, q, k, v, cands, xc, target)
+        assert nplans == 8 + 2 * len(cands) + len(xc) and len(heads) == 2
+    finally:
+        ctx.close()
+    say(f"[gpu] bad candidate reported: {e.value}")
