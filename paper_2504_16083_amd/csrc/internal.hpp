@@ -182,10 +182,10 @@ hipError_t launch_blocks_count(const HeadDev* heads, int nheads, const OpDev* op
                                hipStream_t st);
 // Chooses each head's row stride rho among 1, 2, 4, 8 and the head's
 // rho_alt (smallest total union, ties to the earlier candidate); cand: int64
-// scratch [nheads][NRHO].
+// scratch [nheads][NRHO]; extra: some head has rho_alt candidates.
 constexpr int NRHO = 6;
-hipError_t launch_group_stride(const HeadDev* heads, int nheads, int R, int max_groups, int64_t* cand, int32_t* gcnt,
-                               hipStream_t st);
+hipError_t launch_group_stride(const HeadDev* heads, int nheads, int R, int max_groups, int max_nbq, bool extra,
+                               int64_t* cand, int32_t* gcnt, hipStream_t st);
 hipError_t launch_group_count(const HeadDev* heads, int nheads, const int32_t* gcnt, int max_groups,
                               hipStream_t st);
 // totals[head] = {nnz, gnnz, nitems, nsplit, nparts}

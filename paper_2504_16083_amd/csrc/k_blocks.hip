@@ -364,14 +364,14 @@ __device__ __forceinline__ int rho_candidate(const HeadDev& hd, int c) {
   return c < 4 ? 1 << c : hd.rho_alt[c - 4];
 }
 
-// Union size of every group for every candidate stride (gcnt[head][c][g]),
-// and their per-head totals (cand).
+// Union size of every group for the candidate strides from c0 on
+// (gcnt[head][c][g]), and their per-head totals (cand).
 __global__ __launch_bounds__(256) void k_group_eval(const HeadDev* heads, int R, int64_t* cand, int32_t* gcnt,
-                                                    int max_groups) {
+                                                    int max_groups, int c0) {
   const HeadDev hd = heads[blockIdx.x];
   const int g = blockIdx.y;
   __shared__ int sh;
-  for (int c = 0; c < NRHO; ++c) {
+  for (int c = c0; c < NRHO; ++c) {
     const int rho = rho_candidate(hd, c);
     if (rho <= 0) continue;
     if (g >= groups_for(hd.nbq, R, rho)) continue;      // uniform over the block
@@ -387,6 +387,52 @@ __global__ __launch_bounds__(256) void k_group_eval(const HeadDev* heads, int R,
   }
 }
 
+// The same for row groups of four and the strides 1, 2, 4 and 8 in one pass:
+// those groups lie inside aligned spans of 32 query blocks (span s holds
+// groups 8s .. 8s + 7 of every one of them, group 8s + l starting at block
+// 32s + (l / rho) 4 rho + l mod rho), so each bitmap word of a span is read
+// once for all four strides. One workgroup per (head, span).
+__global__ __launch_bounds__(256) void k_group_eval4(const HeadDev* heads, int64_t* cand, int32_t* gcnt,
+                                                     int max_groups) {
+  const HeadDev hd = heads[blockIdx.x];
+  const int q0 = blockIdx.y * 32;
+  if (q0 >= hd.nbq) return;
+  __shared__ int red[4][32];            // per wave: counts of [stride c][group l]
+  int cnt[32];
+#pragma unroll
+  for (int k = 0; k < 32; ++k) cnt[k] = 0;
+  for (int w = threadIdx.x; w < hd.nwords; w += blockDim.x) {
+    uint32_t x[32];
+#pragma unroll
+    for (int b = 0; b < 32; ++b) x[b] = q0 + b < hd.nbq ? hd.bitmap[(int64_t)(q0 + b) * hd.nwords + w] : 0u;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int rho = 1 << c;
+#pragma unroll
+      for (int l = 0; l < 8; ++l) {
+        const int b0 = (l / rho) * 4 * rho + l % rho;
+        cnt[c * 8 + l] += __popc(x[b0] | x[b0 + rho] | x[b0 + 2 * rho] | x[b0 + 3 * rho]);
+      }
+    }
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int k = 0; k < 32; ++k) {
+    int v = cnt[k];
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    if (lane == 0) red[wave][k] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < 32) {
+    const int k = threadIdx.x, c = k >> 3, g = blockIdx.y * 8 + (k & 7);
+    const int tot = red[0][k] + red[1][k] + red[2][k] + red[3][k];
+    if (g < groups_for(hd.nbq, 4, 1 << c)) {
+      gcnt[((int64_t)blockIdx.x * NRHO + c) * max_groups + g] = tot;
+      atomicAdd(reinterpret_cast<unsigned long long*>(&cand[blockIdx.x * NRHO + c]), (unsigned long long)tot);
+    }
+  }
+}
+
 __global__ void k_group_pick(const HeadDev* heads, int nheads, int R, const int64_t* cand) {
   const int h = blockIdx.x * blockDim.x + threadIdx.x;
   if (h >= nheads) return;
@@ -399,11 +445,18 @@ __global__ void k_group_pick(const HeadDev* heads, int nheads, int R, const int6
   hd.gp[2] = best;
 }
 
-hipError_t launch_group_stride(const HeadDev* heads, int nheads, int R, int max_groups, int64_t* cand,
-                               int32_t* gcnt, hipStream_t st) {
+hipError_t launch_group_stride(const HeadDev* heads, int nheads, int R, int max_groups, int max_nbq, bool extra,
+                               int64_t* cand, int32_t* gcnt, hipStream_t st) {
   if (nheads <= 0 || max_groups <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_zero64, dim3((nheads * NRHO + 255) / 256), dim3(256), 0, st, cand, nheads * NRHO);
-  hipLaunchKernelGGL(k_group_eval, dim3(nheads, max_groups), dim3(256), 0, st, heads, R, cand, gcnt, max_groups);
+  if (R == 4) {
+    hipLaunchKernelGGL(k_group_eval4, dim3(nheads, (max_nbq + 31) / 32), dim3(256), 0, st, heads, cand, gcnt,
+                       max_groups);
+    if (extra)   // the extra strides some heads have
+      hipLaunchKernelGGL(k_group_eval, dim3(nheads, max_groups), dim3(256), 0, st, heads, R, cand, gcnt, max_groups, 4);
+  } else {
+    hipLaunchKernelGGL(k_group_eval, dim3(nheads, max_groups), dim3(256), 0, st, heads, R, cand, gcnt, max_groups, 0);
+  }
   hipLaunchKernelGGL(k_group_pick, dim3((nheads + 63) / 64), dim3(64), 0, st, heads, nheads, R, cand);
   return hipGetLastError();
 }
@@ -507,31 +560,56 @@ hipError_t launch_blocks_scan(const HeadDev* heads, int nheads, int min_chunk, i
   return hipGetLastError();
 }
 
-// Ascending column list of one query block from its bitmap.
+// Words per thread: a bitmap row has at most MMI_MAX_SEQ / 64 / 32 + 8
+// words (one padding block per modality group), so 256 threads need 5.
+constexpr int GF_WORDS = 5;
+
+// Exclusive prefix sum of one count per thread over a 256-thread workgroup,
+// in thread order (wave shuffles, then the wave totals through LDS);
+// *total receives the sum of all.
+__device__ __forceinline__ int block_exclusive_scan(int cnt, int* wtot, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int s = cnt;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int t = __shfl_up(s, off, 64);
+    if (lane >= off) s += t;
+  }
+  if (lane == 63) wtot[wave] = s;
+  __syncthreads();
+  int pre = 0, tot = 0;
+  for (int v = 0; v < 4; ++v) {
+    if (v < wave) pre += wtot[v];
+    tot += wtot[v];
+  }
+  *total = tot;
+  return pre + s - cnt;
+}
+
+// Ascending column list of one query block from its bitmap (each thread's
+// words read once, kept in registers for the write).
 __global__ __launch_bounds__(256) void k_blocks_fill(const HeadDev* heads) {
   const HeadDev hd = heads[blockIdx.x];
   const int qb = blockIdx.y;
   if (qb >= hd.nbq) return;
-  __shared__ int buf[256];
+  __shared__ int wtot[4];
   const uint32_t* gbm = hd.bitmap + (int64_t)qb * hd.nwords;
   const int per = (hd.nwords + 255) / 256;
   const int w0 = threadIdx.x * per;
+  uint32_t x[GF_WORDS];
   int cnt = 0;
-  for (int w = w0; w < min(w0 + per, hd.nwords); ++w) cnt += __popc(gbm[w]);
-  buf[threadIdx.x] = cnt;
-  __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {
-    const int t = (int)threadIdx.x >= off ? buf[threadIdx.x - off] : 0;
-    __syncthreads();
-    buf[threadIdx.x] += t;
-    __syncthreads();
+#pragma unroll
+  for (int k = 0; k < GF_WORDS; ++k) {
+    x[k] = k < per && w0 + k < hd.nwords ? gbm[w0 + k] : 0u;
+    cnt += __popc(x[k]);
   }
-  int pos = hd.rowptr[qb] + buf[threadIdx.x] - cnt;
-  for (int w = w0; w < min(w0 + per, hd.nwords); ++w) {
-    uint32_t v = gbm[w];
+  int total;
+  int pos = hd.rowptr[qb] + block_exclusive_scan(cnt, wtot, &total);
+#pragma unroll
+  for (int k = 0; k < GF_WORDS; ++k) {
+    uint32_t v = x[k];
     while (v) {
       const int b = __ffs(v) - 1;
-      hd.col[pos++] = w * 32 + b;
+      hd.col[pos++] = (w0 + k) * 32 + b;
       v &= v - 1;
     }
   }
@@ -550,7 +628,7 @@ __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R)
   const int gr = blockIdx.y;
   if (gr >= hd.gp[1]) return;
   const int rho = hd.gp[0];
-  __shared__ int buf[256];
+  __shared__ int wtot[2][4];
   __shared__ int qmin[4];
   int rows[4];
   for (int r = 0; r < 4; ++r) rows[r] = r < R ? group_row(gr, r, R, rho) : hd.nbq;
@@ -563,37 +641,40 @@ __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R)
     const int p = hd.qperm ? hd.qperm[slot] : (slot < hd.S ? slot : -1);
     if (p >= 0) atomicMin(&qmin[r], hd.causal ? p : INT_BIG - 1);   // bidirectional: only padding masks
   }
+  // this thread's words of the members' bitmaps, read once for both passes
   const int per = (hd.nwords + 255) / 256;
   const int w0 = threadIdx.x * per;
+  uint32_t bits[GF_WORDS][4];
   int cntA = 0, cntB = 0;        // entries every member selects / the others
-  for (int w = w0; w < min(w0 + per, hd.nwords); ++w) {
+#pragma unroll
+  for (int k = 0; k < GF_WORDS; ++k) {
+    const int w = w0 + k;
+    const bool in = k < per && w < hd.nwords;
     uint32_t u = 0, a = 0xffffffffu;
-    for (int r = 0; r < R; ++r)
-      if (rows[r] < hd.nbq) { const uint32_t x = hd.bitmap[(int64_t)rows[r] * hd.nwords + w]; u |= x; a &= x; }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      bits[k][r] = in && rows[r] < hd.nbq ? hd.bitmap[(int64_t)rows[r] * hd.nwords + w] : 0u;
+      if (rows[r] < hd.nbq) a &= bits[k][r];
+      u |= bits[k][r];
+    }
     a &= u;
     cntA += __popc(a);
     cntB += __popc(u & ~a);
   }
-  __shared__ int bufB[256];
-  buf[threadIdx.x] = cntA;
-  bufB[threadIdx.x] = cntB;
-  __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {
-    const int t = (int)threadIdx.x >= off ? buf[threadIdx.x - off] : 0;
-    const int tb = (int)threadIdx.x >= off ? bufB[threadIdx.x - off] : 0;
-    __syncthreads();
-    buf[threadIdx.x] += t;
-    bufB[threadIdx.x] += tb;
-    __syncthreads();
-  }
-  int posA = hd.growptr[gr] + buf[threadIdx.x] - cntA;
-  int posB = hd.growptr[gr] + buf[255] + bufB[threadIdx.x] - cntB;
-  for (int w = w0; w < min(w0 + per, hd.nwords); ++w) {
-    uint32_t bits[4] = {0, 0, 0, 0};
+  // exclusive prefix sums of both counts over the workgroup in thread order
+  int totA, totB;
+  const int preA = block_exclusive_scan(cntA, wtot[0], &totA);
+  const int preB = block_exclusive_scan(cntB, wtot[1], &totB);
+  int posA = hd.growptr[gr] + preA;
+  int posB = hd.growptr[gr] + totA + preB;
+#pragma unroll
+  for (int k = 0; k < GF_WORDS; ++k) {
+    const int w = w0 + k;
     uint32_t u = 0, a = 0xffffffffu;
-    for (int r = 0; r < R; ++r) {
-      if (rows[r] < hd.nbq) { bits[r] = hd.bitmap[(int64_t)rows[r] * hd.nwords + w]; a &= bits[r]; }
-      u |= bits[r];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      if (rows[r] < hd.nbq) a &= bits[k][r];
+      u |= bits[k][r];
     }
     a &= u;
     while (u) {
@@ -603,8 +684,9 @@ __global__ __launch_bounds__(256) void k_group_fill(const HeadDev* heads, int R)
       if (hd.kmaxpos) kmax = hd.kmaxpos[j];
       else kmax = j * B + B - 1 < hd.S ? j * B + B - 1 : INT_BIG;
       uint32_t flags = 0;
-      for (int r = 0; r < R; ++r) {
-        const uint32_t sel = (bits[r] >> b) & 1u;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint32_t sel = (bits[k][r] >> b) & 1u;
         flags |= sel << (16 + r);
         if (sel && kmax > qmin[r]) flags |= 1u << (24 + r);
       }

@@ -848,7 +848,9 @@ static void plan_create_impl(mmi_ctx* ctx, const mmi_problem* prob_in, const mmi
   HIPCHK(launch_blocks_count(P->d_heads, p.Hq, P->d_ops, g, max_nbq, st));
   int64_t* d_cand = dalloc<int64_t>(P, (size_t)p.Hq * NRHO);
   int32_t* d_gcnt = dalloc<int32_t>(P, (size_t)p.Hq * NRHO * std::max(max_groups, 1));
-  HIPCHK(launch_group_stride(P->d_heads, p.Hq, R, max_groups, d_cand, d_gcnt, st));
+  bool extra_rho = false;
+  for (const HeadDev& hd : P->heads) extra_rho = extra_rho || hd.rho_alt[0] > 0 || hd.rho_alt[1] > 0;
+  HIPCHK(launch_group_stride(P->d_heads, p.Hq, R, max_groups, max_nbq, extra_rho, d_cand, d_gcnt, st));
   HIPCHK(launch_group_count(P->d_heads, p.Hq, d_gcnt, max_groups, st));
   const size_t ntot = (size_t)p.Hq * NTOT;
   int64_t* d_tot = dalloc<int64_t>(P, ntot);
