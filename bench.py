@@ -41,7 +41,7 @@ FLOP_PER_BLOCK = 4 * 64 * 64 * 128
 # reported as null.
 TRAFFIC_SOURCES = ("k_attention.hip", "k_blocks.hip", "runtime.hip")
 TRAFFIC = {
-    "b92e6c72ce421555": {"workload": "cfg4_mm_1m", "fetch_kib": 550438671, "write_kib": 7698748,
+    "b01aa7b3395f3a7b": {"workload": "cfg4_mm_1m", "fetch_kib": 542877060, "write_kib": 7698770,
                          "fetch_scale": 1.939, "write_scale": 1.000},
 }
 
